@@ -1,0 +1,231 @@
+/*
+ * cc.h -- C ABI of the counter-causal refresh-scoring library (libcc.so, gfx950).
+ *
+ * The library implements the memory-refresh cycle of counter-causal KV-cache
+ * eviction (Gould & van den Hengel, "Back from the Future: Key-Value Cache
+ * Management by Counter-Causal Surprise"):
+ *
+ *   cc_score        per-entry surprise scores of the cached tokens (Sec. 3.1):
+ *                   attention over the stored keys/values under the
+ *                   counter-causal mask, the output projection, the LM head and
+ *                   the log-softmax at the cached token id;
+ *   cc_select_keep  the k highest-scoring entries of each segment (Sec. 3.2,
+ *                   memory refresh: argsort and keep the top J);
+ *   cc_compact_kv   gather the kept entries of the KV cache, token ids and
+ *                   position ids (Sec. 3.2, memory refresh: K', V', X updates).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are device pointers unless the name ends in _h (host memory).
+ *   - Every call only enqueues work on `stream` (a hipStream_t; NULL is the
+ *     default stream) and returns; results are ready when the stream is.
+ *     Host arrays (_h) are read before the call returns.
+ *   - The caller owns every buffer.  The library allocates no device memory;
+ *     scratch space comes from the caller's workspace, whose size the matching
+ *     *_workspace query returns (a NULL workspace with size 0 is valid when the
+ *     query returned 0).  Small planning tables are copied from host memory
+ *     into the workspace on `stream`.
+ *   - Arguments are checked on the host before anything is enqueued.  A call
+ *     that returns a status other than CC_OK has enqueued nothing and written
+ *     nothing.  Faults inside kernels surface at the caller's next
+ *     synchronisation.  Token ids outside [0, vocab) and position ids outside
+ *     the cache are a caller error with undefined results for that row.
+ *   - Element types: CC_BF16 tensors are bfloat16, CC_F32 tensors are float32;
+ *     scores are always float32.  Matrices are row-major.
+ *   - Calls that share a workspace must be ordered (same stream or synchronised).
+ */
+#ifndef CC_H
+#define CC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cc_status {
+  CC_OK = 0,
+  CC_ERR_ARG = 1,          /* a NULL required pointer, a bad enum value, a bad count */
+  CC_ERR_SHAPE = 2,        /* inconsistent sizes (e.g. n_heads_q % n_heads_kv != 0) */
+  CC_ERR_DTYPE = 3,        /* dtype not valid for this call */
+  CC_ERR_WORKSPACE = 4,    /* workspace smaller than the query returned */
+  CC_ERR_UNSUPPORTED = 5,  /* a valid problem this build has no kernel for */
+  CC_ERR_HIP = 6           /* the HIP runtime rejected a launch or copy */
+} cc_status;
+
+typedef enum cc_dtype { CC_F32 = 0, CC_BF16 = 1 } cc_dtype;
+
+/* Counter-causal mask (Sec. 3.1): position i attends to cache positions j > i of
+ * its own sequence (STRICT, the paper's mask).  INCLUSIVE (j >= i) is provided for
+ * testing.  A row with no allowed key has a zero attention output. */
+typedef enum cc_diag { CC_DIAG_STRICT = 0, CC_DIAG_INCLUSIVE = 1 } cc_diag;
+
+/* LAST_LAYER: the fast single-layer approximation (Sec. 3.1): queries are given,
+ * attention runs on the cache's last layer, then W_o and the LM head.
+ * FULL: every layer runs with fresh queries from the token embeddings against the
+ * stored keys/values of that layer (Sec. 3.1, full counter-causal pass). */
+typedef enum cc_mode { CC_MODE_LAST_LAYER = 0, CC_MODE_FULL = 1 } cc_mode;
+
+typedef enum cc_kv_layout { CC_KV_CONTIGUOUS = 0, CC_KV_PAGED = 1 } cc_kv_layout;
+
+/* A view of the KV cache (keys and values share the layout).  head_dim elements of
+ * one (layer, KV head, token) are contiguous; strides are in elements.
+ *   CONTIGUOUS: element (seq b, layer l, head h, token t, e) is at
+ *       base + b*seq_stride + l*layer_stride + h*head_stride + t*tok_stride + e
+ *   PAGED: token t of sequence b lives in page block_table[b*max_pages + t/page_size],
+ *       slot t % page_size:
+ *       base + l*layer_stride + page*page_stride + h*head_stride + slot*tok_stride + e
+ * Token t is the t-th cached entry of its sequence in cache order (ascending
+ * original position after any number of refreshes). */
+typedef struct cc_kv {
+  int32_t layout;              /* cc_kv_layout */
+  int32_t n_layers;            /* layers held by the cache */
+  void* k;                     /* device base of keys */
+  void* v;                     /* device base of values */
+  int64_t seq_stride;          /* CONTIGUOUS only */
+  int64_t layer_stride;
+  int64_t head_stride;
+  int64_t tok_stride;
+  int64_t page_stride;         /* PAGED only */
+  const int32_t* block_table;  /* PAGED only: device [n_seqs][max_pages] page ids */
+  int32_t page_size;           /* PAGED only: tokens per page, a power of two >= 16 */
+  int32_t max_pages;           /* PAGED only: row length of block_table */
+} cc_kv;
+
+/* Shape of one refresh.  Sequences are ragged: sequence b holds cache entries
+ * [cu_seqlens[b], cu_seqlens[b+1]) of every token-major array (N = cu_seqlens[n_seqs]).
+ * With GQA, query head h reads KV head h / (n_heads_q / n_heads_kv). */
+typedef struct cc_problem {
+  int32_t dtype;               /* cc_dtype of q, k, v and all weights */
+  int32_t mode;                /* cc_mode */
+  int32_t diag;                /* cc_diag */
+  int32_t n_seqs;              /* >= 1 */
+  const int32_t* cu_seqlens_h; /* host [n_seqs+1], cu[0] = 0, non-decreasing */
+  const int32_t* cu_seqlens_d; /* the same values in device memory */
+  int32_t n_heads_q;
+  int32_t n_heads_kv;          /* divides n_heads_q */
+  int32_t head_dim;            /* 64 or 128 */
+  int32_t hidden;              /* D: model width, rows of W_o */
+  int32_t vocab;               /* V: rows of the LM head */
+  int32_t n_layers;            /* FULL only: transformer layers (<= kv.n_layers) */
+  int32_t ffn;                 /* FULL only: SwiGLU width */
+  float softmax_scale;         /* 0 selects 1/sqrt(head_dim) (Eq. (2)) */
+  float rope_theta;            /* FULL only: rotary base */
+  float rms_eps;               /* FULL only: RMSNorm epsilon */
+  int32_t n_frozen;            /* first n_frozen entries of each sequence are sink
+                                  slots that are never evicted (score +inf) */
+} cc_problem;
+
+/* Weights of one transformer layer (FULL mode), device pointers in `dtype`. */
+typedef struct cc_layer_weights {
+  const void* attn_norm;       /* [D] RMSNorm gain before attention */
+  const void* wq;              /* [Hq*d][D] query projection */
+  const void* wo;              /* [D][Hq*d] output projection */
+  const void* mlp_norm;        /* [D] RMSNorm gain before the MLP */
+  const void* w_gate;          /* [F][D] */
+  const void* w_up;            /* [F][D] */
+  const void* w_down;          /* [D][F] */
+} cc_layer_weights;
+
+typedef struct cc_inputs {
+  const void* q;               /* LAST_LAYER: [N][Hq][d] queries (already rotated) */
+  cc_kv kv;                    /* LAST_LAYER scores layer kv.n_layers-1; FULL uses
+                                  layers 0..n_layers-1 (keys already rotated) */
+  const int32_t* token_ids;    /* [N] cached token ids X */
+  const int32_t* pos_ids;      /* FULL: [N] original positions, NULL -> 0..n_b-1 */
+  const void* w_o;             /* LAST_LAYER: [D][Hq*d] */
+  const void* w_lm;            /* [V][D] LM head */
+  const void* embed;           /* FULL: [V][D] token embeddings */
+  const cc_layer_weights* layers_h; /* FULL: host array [n_layers] */
+  const void* final_norm;      /* FULL: [D] final RMSNorm gain */
+} cc_inputs;
+
+/* Human-readable name of a status code (static string). */
+const char* cc_status_str(cc_status s);
+
+/* Library build identifier, e.g. "libcc gfx950 <date>". */
+const char* cc_version(void);
+
+/* ------------------------------------------------------------------ scoring */
+
+/* Workspace bytes cc_score needs for problem p (sizes only; pointers unused). */
+cc_status cc_score_workspace(const cc_problem* p, size_t* bytes);
+
+/* Surprise score of every cached entry (Eq. (5), Sec. 3.1):
+ *   scores[i] = logsumexp_v(z_i) - z_i[x_i] = -log P(x_i | x_{i+1..n_b-1}),
+ * a strictly decreasing function of P, where z_i are the LM-head logits of entry i
+ * after the counter-causal pass.  The last entry of each sequence (no future) and
+ * the first n_frozen entries score +inf.  scores: device float32 [N].
+ * The [N][V] logits are never materialised. */
+cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sub-steps of cc_score, exposed for testing and measurement. */
+
+/* Workspace for cc_attention_cc. */
+cc_status cc_attention_workspace(const cc_problem* p, size_t* bytes);
+
+/* Counter-causal attention (Eq. (2) under the mask of Sec. 3.1) over cache layer
+ * `layer`: o[i][h][:] = sum_{j allowed} softmax_j(scale * q[i][h].k[j][c]) v[j][c],
+ * c = h / g.  q, o: [N][Hq][d] in dtype (o may not alias q). */
+cc_status cc_attention_cc(const cc_problem* p, const void* q, const cc_kv* kv,
+                          int32_t layer, void* o, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* Workspace for cc_lmhead_score. */
+cc_status cc_lmhead_workspace(const cc_problem* p, size_t* bytes);
+
+/* LM head, log-softmax and target gather (Eq. (5)): for hidden rows u [N][D]
+ * (dtype), scores[i] = logsumexp(W_lm u_i) - (W_lm u_i)[ids[i]], with the
+ * last-entry / frozen rule applied.  lse (nullable) receives logsumexp. */
+cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
+                          const int32_t* token_ids, float* scores, float* lse,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Dense projection y[m][n] = sum_k x[m][k] w[n][k] (x: [M][K], w: [N][K], y: [M][N],
+ * all in dtype), the layer's output projection of the fast variant. */
+cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_t M,
+                    int32_t N, int32_t K, void* stream);
+
+/* ------------------------------------------------------------------ selection */
+
+/* Workspace for cc_select_keep with n_segs segments. */
+cc_status cc_select_workspace(int32_t n_segs, size_t* bytes);
+
+/* Keep selection (Sec. 3.2): segment s is scores[seg_start_h[s] .. +seg_len_h[s]).
+ * Its k = k_h[s] kept entries are the first k under the order (score descending,
+ * -0 == +0, NaN below -inf; ties to the lower index), written in ascending order as
+ * segment-local indices to keep_idx[off_s .. off_s + k), off_s = sum_{t<s} k_h[t].
+ * 0 <= k <= seg_len.  Segments may overlap (e.g. one per KV head over the same
+ * per-token scores).  keep_idx: device int32 [sum k]. */
+cc_status cc_select_keep(const float* scores, int32_t n_segs, const int64_t* seg_start_h,
+                         const int32_t* seg_len_h, const int32_t* k_h, int32_t* keep_idx,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ compaction */
+
+/* Workspace for cc_compact_kv on a cache of cache_layers layers. */
+cc_status cc_compact_workspace(const cc_problem* p, int32_t cache_layers, int32_t per_head,
+                               size_t* bytes);
+
+/* KV compaction (Sec. 3.2): for every cache layer, KV head and sequence b,
+ *   dst[j] = src[keep[j]] for j < k_b   (a bit copy of head_dim elements),
+ * with keep the list from cc_select_keep.  Lists are packed back to back:
+ * per_head = 0: one list per sequence (k_h[b]); per_head = 1: one list per
+ * (sequence, KV head) in order b*n_heads_kv + h (k_h[b*Hkv+h]).
+ * dst is `out` (same geometry as `kv`) or, when out is NULL, `kv` itself (in
+ * place; safe because lists are ascending so keep[j] >= j).  token_ids and pos_ids
+ * (nullable, device int32 [N], token-major by cu_seqlens) are compacted in place
+ * with the first list of each sequence: ids[cu_b + j] = ids[cu_b + keep[j]].
+ * Entries at and past k_b are left untouched (paged: pages past ceil(k_b/P) are free
+ * for the caller to reuse). */
+cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* keep_idx,
+                        const int32_t* k_h, int32_t per_head, int32_t* token_ids,
+                        int32_t* pos_ids, const cc_kv* out, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CC_H */

@@ -1,0 +1,484 @@
+// C ABI of libcc: argument validation, planning (grids, work lists, workspace layout)
+// and kernel launches for the refresh-scoring pass.  Host code only; every kernel lives
+// in its own translation unit behind the launchers declared in cc_internal.h.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "cc_internal.h"
+
+using namespace cc;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+int esize(int dtype) { return dtype == CC_BF16 ? 2 : 4; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+#define CC_TRY(x)                       \
+  do {                                  \
+    cc_status _st = (x);                \
+    if (_st != CC_OK) return _st;       \
+  } while (0)
+
+#define CC_HIP(x)                                   \
+  do {                                              \
+    if ((x) != hipSuccess) return CC_ERR_HIP;       \
+  } while (0)
+
+cc_status check_problem(const cc_problem* p) {
+  if (!p) return CC_ERR_ARG;
+  if (p->dtype != CC_F32 && p->dtype != CC_BF16) return CC_ERR_DTYPE;
+  if (p->mode != CC_MODE_LAST_LAYER && p->mode != CC_MODE_FULL) return CC_ERR_ARG;
+  if (p->diag != CC_DIAG_STRICT && p->diag != CC_DIAG_INCLUSIVE) return CC_ERR_ARG;
+  if (p->n_seqs < 1 || !p->cu_seqlens_h || !p->cu_seqlens_d) return CC_ERR_ARG;
+  if (p->cu_seqlens_h[0] != 0) return CC_ERR_SHAPE;
+  for (int b = 0; b < p->n_seqs; ++b)
+    if (p->cu_seqlens_h[b + 1] < p->cu_seqlens_h[b]) return CC_ERR_SHAPE;
+  if (p->n_heads_q < 1 || p->n_heads_kv < 1) return CC_ERR_SHAPE;
+  if (p->n_heads_q % p->n_heads_kv != 0) return CC_ERR_SHAPE;
+  if (p->head_dim < 1 || p->hidden < 1 || p->vocab < 1) return CC_ERR_SHAPE;
+  if (p->n_frozen < 0) return CC_ERR_ARG;
+  if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.f) return CC_ERR_ARG;
+  if (p->dtype == CC_BF16) {
+    if (p->head_dim != 128) return CC_ERR_UNSUPPORTED;
+    if (p->hidden % 64 != 0) return CC_ERR_UNSUPPORTED;
+  } else {
+    if (p->head_dim != 64 && p->head_dim != 128) return CC_ERR_UNSUPPORTED;
+  }
+  if (p->mode == CC_MODE_FULL) {
+    if (p->n_layers < 1 || p->ffn < 1) return CC_ERR_SHAPE;
+    if (p->dtype != CC_BF16) return CC_ERR_UNSUPPORTED;
+    if (p->ffn % 64 != 0) return CC_ERR_UNSUPPORTED;
+    if (!(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return CC_ERR_ARG;
+  }
+  return CC_OK;
+}
+
+int n_tokens(const cc_problem* p) { return p->cu_seqlens_h[p->n_seqs]; }
+int max_len(const cc_problem* p) {
+  int m = 0;
+  for (int b = 0; b < p->n_seqs; ++b) m = std::max(m, p->cu_seqlens_h[b + 1] - p->cu_seqlens_h[b]);
+  return m;
+}
+
+cc_status check_kv(const cc_problem* p, const cc_kv* kv, int min_layers) {
+  if (!kv || !kv->k || !kv->v) return CC_ERR_ARG;
+  if (kv->layout != CC_KV_CONTIGUOUS && kv->layout != CC_KV_PAGED) return CC_ERR_ARG;
+  if (kv->n_layers < min_layers) return CC_ERR_SHAPE;
+  if (kv->layer_stride < 0 || kv->head_stride < 0 || kv->tok_stride < p->head_dim)
+    return CC_ERR_SHAPE;
+  const int es = esize(p->dtype);
+  if (!aligned16(kv->k) || !aligned16(kv->v)) return CC_ERR_ARG;
+  auto str_ok = [&](int64_t s) { return (s * es) % 16 == 0; };
+  if (!str_ok(kv->layer_stride) || !str_ok(kv->head_stride) || !str_ok(kv->tok_stride))
+    return CC_ERR_UNSUPPORTED;
+  if (kv->layout == CC_KV_PAGED) {
+    if (!kv->block_table || !is_pow2(kv->page_size) || kv->page_size < 16) return CC_ERR_ARG;
+    if (kv->page_stride < 0 || !str_ok(kv->page_stride)) return CC_ERR_UNSUPPORTED;
+    const int need = (max_len(p) + kv->page_size - 1) / kv->page_size;
+    if (kv->max_pages < need) return CC_ERR_SHAPE;
+  } else {
+    if (kv->seq_stride < 0 || !str_ok(kv->seq_stride)) return CC_ERR_UNSUPPORTED;
+  }
+  return CC_OK;
+}
+
+// Address view for kernels; byte_strides = true multiplies strides by the element size.
+KvView make_view(const cc_kv* kv, const void* base, int es_mult) {
+  KvView v;
+  v.base = base;
+  v.seq_stride = kv->seq_stride * es_mult;
+  v.layer_stride = kv->layer_stride * es_mult;
+  v.head_stride = kv->head_stride * es_mult;
+  v.tok_stride = kv->tok_stride * es_mult;
+  v.page_stride = kv->page_stride * es_mult;
+  v.block_table = kv->block_table;
+  int shift = 0;
+  if (kv->layout == CC_KV_PAGED)
+    while ((1 << shift) < kv->page_size) ++shift;
+  v.page_shift = shift;
+  v.page_mask = kv->layout == CC_KV_PAGED ? kv->page_size - 1 : 0;
+  v.max_pages = kv->max_pages;
+  v.pad = 0;
+  return v;
+}
+
+float softmax_scale(const cc_problem* p) {
+  return p->softmax_scale > 0.f ? p->softmax_scale : 1.f / std::sqrt(float(p->head_dim));
+}
+
+// Attention work items, heaviest first: an item's cost is the number of keys its first
+// row may attend to, n_b - first position.
+std::vector<int4> attention_work(const cc_problem* p) {
+  const int rows_item = attention_rows_per_item(p->dtype, p->head_dim);
+  const int g = p->n_heads_q / p->n_heads_kv;
+  std::vector<int4> items;
+  std::vector<int64_t> cost;
+  for (int b = 0; b < p->n_seqs; ++b) {
+    const int n = p->cu_seqlens_h[b + 1] - p->cu_seqlens_h[b];
+    const int64_t rows = int64_t(n) * g;
+    const int nrb = int((rows + rows_item - 1) / rows_item);
+    for (int rb = 0; rb < nrb; ++rb)
+      for (int h = 0; h < p->n_heads_kv; ++h) {
+        items.push_back(make_int4(b, h, rb, 0));
+        cost.push_back(n - int64_t(rb) * rows_item / g);
+      }
+  }
+  std::vector<int> idx(items.size());
+  for (size_t i = 0; i < idx.size(); ++i) idx[i] = int(i);
+  std::stable_sort(idx.begin(), idx.end(), [&](int a, int c) { return cost[a] > cost[c]; });
+  std::vector<int4> out(items.size());
+  for (size_t i = 0; i < idx.size(); ++i) out[i] = items[idx[i]];
+  return out;
+}
+
+size_t attention_ws_bytes(const cc_problem* p) {
+  const int rows_item = attention_rows_per_item(p->dtype, p->head_dim);
+  const int g = p->n_heads_q / p->n_heads_kv;
+  size_t items = 0;
+  for (int b = 0; b < p->n_seqs; ++b) {
+    const int64_t n = p->cu_seqlens_h[b + 1] - p->cu_seqlens_h[b];
+    items += size_t((n * g + rows_item - 1) / rows_item) * p->n_heads_kv;
+  }
+  return align_up(items * sizeof(int4));
+}
+
+size_t lmhead_ws_bytes(const cc_problem* p) {
+  const size_t N = n_tokens(p);
+  const int vt = lmhead_vocab_tile(p->dtype);
+  const size_t n_vt = (p->vocab + vt - 1) / vt;
+  return align_up(n_vt * N * sizeof(float2)) + align_up(N * sizeof(float));
+}
+
+struct ScoreLayout {
+  size_t attn, o, u, lm, total;
+};
+
+ScoreLayout score_layout(const cc_problem* p) {
+  ScoreLayout L;
+  const size_t N = n_tokens(p), es = esize(p->dtype);
+  size_t off = 0;
+  L.attn = off;
+  off += attention_ws_bytes(p);
+  L.o = off;
+  off += align_up(N * p->n_heads_q * p->head_dim * es);
+  L.u = off;
+  off += align_up(N * p->hidden * es);
+  L.lm = off;
+  off += lmhead_ws_bytes(p);
+  L.total = off;
+  return L;
+}
+
+char* at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+cc_status run_attention(const cc_problem* p, const void* q, const cc_kv* kv, int layer, void* o,
+                        void* ws, hipStream_t s) {
+  std::vector<int4> work = attention_work(p);
+  if (work.empty()) return CC_OK;
+  CC_HIP(hipMemcpyAsync(ws, work.data(), work.size() * sizeof(int4), hipMemcpyHostToDevice, s));
+  AttnLaunch a;
+  a.dtype = p->dtype;
+  a.q = q;
+  a.o = o;
+  a.cu_d = p->cu_seqlens_d;
+  a.work_d = static_cast<const int4*>(ws);
+  a.n_work = int(work.size());
+  a.k = make_view(kv, kv->k, 1);
+  a.v = make_view(kv, kv->v, 1);
+  a.paged = kv->layout == CC_KV_PAGED;
+  a.layer = layer;
+  a.n_heads_q = p->n_heads_q;
+  a.n_heads_kv = p->n_heads_kv;
+  a.head_dim = p->head_dim;
+  a.scale = softmax_scale(p);
+  a.inclusive = p->diag == CC_DIAG_INCLUSIVE;
+  CC_HIP(launch_attention(a, s));
+  return CC_OK;
+}
+
+cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const int32_t* ids,
+                     float* scores, float* lse, void* ws, hipStream_t s) {
+  const int N = n_tokens(p);
+  const int vt = lmhead_vocab_tile(p->dtype);
+  const size_t n_vt = (p->vocab + vt - 1) / vt;
+  LmHeadLaunch a;
+  a.dtype = p->dtype;
+  a.u = u;
+  a.w_lm = w_lm;
+  a.ids = ids;
+  a.scores = scores;
+  a.lse = lse;
+  a.partial = reinterpret_cast<float2*>(ws);
+  a.target = reinterpret_cast<float*>(at(ws, align_up(n_vt * N * sizeof(float2))));
+  a.cu_d = p->cu_seqlens_d;
+  a.n_seqs = p->n_seqs;
+  a.N = N;
+  a.D = p->hidden;
+  a.V = p->vocab;
+  a.n_frozen = p->n_frozen;
+  CC_HIP(launch_lmhead(a, s));
+  return CC_OK;
+}
+
+cc_status check_ws(void* ws, size_t have, size_t need) {
+  if (have < need) return CC_ERR_WORKSPACE;
+  if (need > 0 && !ws) return CC_ERR_ARG;
+  if (need > 0 && (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0) return CC_ERR_ARG;
+  return CC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cc_status_str(cc_status s) {
+  switch (s) {
+    case CC_OK: return "CC_OK";
+    case CC_ERR_ARG: return "CC_ERR_ARG: invalid argument";
+    case CC_ERR_SHAPE: return "CC_ERR_SHAPE: inconsistent sizes";
+    case CC_ERR_DTYPE: return "CC_ERR_DTYPE: unsupported dtype for this call";
+    case CC_ERR_WORKSPACE: return "CC_ERR_WORKSPACE: workspace too small";
+    case CC_ERR_UNSUPPORTED: return "CC_ERR_UNSUPPORTED: no kernel for this shape";
+    case CC_ERR_HIP: return "CC_ERR_HIP: HIP runtime error";
+  }
+  return "unknown cc_status";
+}
+
+const char* cc_version(void) { return "libcc gfx950 " __DATE__; }
+
+cc_status cc_attention_workspace(const cc_problem* p, size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  *bytes = attention_ws_bytes(p);
+  return CC_OK;
+}
+
+cc_status cc_attention_cc(const cc_problem* p, const void* q, const cc_kv* kv, int32_t layer,
+                          void* o, void* ws, size_t ws_bytes, void* stream) {
+  CC_TRY(check_problem(p));
+  CC_TRY(check_kv(p, kv, 1));
+  if (layer < 0 || layer >= kv->n_layers) return CC_ERR_ARG;
+  if (n_tokens(p) > 0 && (!q || !o)) return CC_ERR_ARG;
+  if (p->dtype == CC_BF16 && (!aligned16(q) || !aligned16(o))) return CC_ERR_ARG;
+  CC_TRY(check_ws(ws, ws_bytes, attention_ws_bytes(p)));
+  return run_attention(p, q, kv, layer, o, ws, static_cast<hipStream_t>(stream));
+}
+
+cc_status cc_lmhead_workspace(const cc_problem* p, size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  *bytes = lmhead_ws_bytes(p);
+  return CC_OK;
+}
+
+cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
+                          const int32_t* token_ids, float* scores, float* lse, void* ws,
+                          size_t ws_bytes, void* stream) {
+  CC_TRY(check_problem(p));
+  if (n_tokens(p) > 0 && (!u || !w_lm || !token_ids || !scores)) return CC_ERR_ARG;
+  if (p->dtype == CC_BF16 && (!aligned16(u) || !aligned16(w_lm))) return CC_ERR_ARG;
+  CC_TRY(check_ws(ws, ws_bytes, lmhead_ws_bytes(p)));
+  return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream));
+}
+
+cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N,
+                    int32_t K, void* stream) {
+  if (dtype != CC_F32 && dtype != CC_BF16) return CC_ERR_DTYPE;
+  if (M < 0 || N < 0 || K < 1) return CC_ERR_SHAPE;
+  if (M > 0 && N > 0 && (!x || !w || !y)) return CC_ERR_ARG;
+  if (dtype == CC_BF16) {
+    if (K % 64 != 0) return CC_ERR_UNSUPPORTED;
+    if (!aligned16(x) || !aligned16(w)) return CC_ERR_ARG;
+  }
+  CC_HIP(launch_linear(dtype, x, w, y, M, N, K, static_cast<hipStream_t>(stream)));
+  return CC_OK;
+}
+
+cc_status cc_score_workspace(const cc_problem* p, size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  if (p->mode == CC_MODE_FULL) return CC_ERR_UNSUPPORTED;
+  *bytes = score_layout(p).total;
+  return CC_OK;
+}
+
+cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void* ws,
+                   size_t ws_bytes, void* stream) {
+  CC_TRY(check_problem(p));
+  if (!in) return CC_ERR_ARG;
+  if (p->mode == CC_MODE_FULL) return CC_ERR_UNSUPPORTED;
+  CC_TRY(check_kv(p, &in->kv, 1));
+  const int N = n_tokens(p);
+  if (N > 0 && (!in->q || !in->w_o || !in->w_lm || !in->token_ids || !scores)) return CC_ERR_ARG;
+  if (p->dtype == CC_BF16 && (!aligned16(in->q) || !aligned16(in->w_o) || !aligned16(in->w_lm)))
+    return CC_ERR_ARG;
+  const ScoreLayout L = score_layout(p);
+  CC_TRY(check_ws(ws, ws_bytes, L.total));
+  if (N == 0) return CC_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* o = at(ws, L.o);
+  void* u = at(ws, L.u);
+  CC_TRY(run_attention(p, in->q, &in->kv, in->kv.n_layers - 1, o, at(ws, L.attn), s));
+  CC_HIP(launch_linear(p->dtype, o, in->w_o, u, N, p->hidden, p->n_heads_q * p->head_dim, s));
+  return run_lmhead(p, u, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+}
+
+// ------------------------------------------------------------------ selection
+
+cc_status cc_select_workspace(int32_t n_segs, size_t* bytes) {
+  if (!bytes || n_segs < 0) return CC_ERR_ARG;
+  *bytes = align_up(size_t(n_segs) * sizeof(SelSeg));
+  return CC_OK;
+}
+
+cc_status cc_select_keep(const float* scores, int32_t n_segs, const int64_t* seg_start_h,
+                         const int32_t* seg_len_h, const int32_t* k_h, int32_t* keep_idx,
+                         void* ws, size_t ws_bytes, void* stream) {
+  if (n_segs < 0) return CC_ERR_ARG;
+  if (n_segs == 0) return CC_OK;
+  if (!seg_start_h || !seg_len_h || !k_h) return CC_ERR_ARG;
+  std::vector<SelSeg> segs(n_segs);
+  int64_t out = 0;
+  int mx = 0;
+  bool any_len = false;
+  for (int i = 0; i < n_segs; ++i) {
+    if (seg_len_h[i] < 0 || seg_start_h[i] < 0) return CC_ERR_SHAPE;
+    if (k_h[i] < 0 || k_h[i] > seg_len_h[i]) return CC_ERR_SHAPE;
+    segs[i].start = seg_start_h[i];
+    segs[i].len = seg_len_h[i];
+    segs[i].k = k_h[i];
+    segs[i].out = out;
+    out += k_h[i];
+    mx = std::max(mx, seg_len_h[i]);
+    any_len = any_len || (k_h[i] > 0);
+  }
+  if (any_len && (!scores || !keep_idx)) return CC_ERR_ARG;
+  CC_TRY(check_ws(ws, ws_bytes, align_up(size_t(n_segs) * sizeof(SelSeg))));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  CC_HIP(hipMemcpyAsync(ws, segs.data(), segs.size() * sizeof(SelSeg), hipMemcpyHostToDevice, s));
+  CC_HIP(launch_select(scores, static_cast<const SelSeg*>(ws), n_segs, mx, keep_idx, s));
+  return CC_OK;
+}
+
+// ------------------------------------------------------------------ compaction
+
+namespace {
+struct CompactPlan {
+  std::vector<CompactList> lists;
+  std::vector<CompactPlane> planes;
+  std::vector<int32_t> seq_list;
+  int max_k = 0;
+  size_t off_lists = 0, off_planes = 0, off_seq = 0, total = 0;
+};
+
+size_t compact_ws_bytes_for(const cc_problem* p, int per_head, int n_layers) {
+  const size_t n_lists = size_t(p->n_seqs) * (per_head ? p->n_heads_kv : 1);
+  const size_t n_planes = size_t(p->n_seqs) * n_layers * p->n_heads_kv;
+  return align_up(n_lists * sizeof(CompactList)) + align_up(n_planes * sizeof(CompactPlane)) +
+         align_up(size_t(p->n_seqs) * sizeof(int32_t));
+}
+}  // namespace
+
+cc_status cc_compact_workspace(const cc_problem* p, int32_t cache_layers, int32_t per_head,
+                               size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  if (per_head != 0 && per_head != 1) return CC_ERR_ARG;
+  if (cache_layers < 1) return CC_ERR_ARG;
+  *bytes = compact_ws_bytes_for(p, per_head, cache_layers);
+  return CC_OK;
+}
+
+cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* keep_idx,
+                        const int32_t* k_h, int32_t per_head, int32_t* token_ids,
+                        int32_t* pos_ids, const cc_kv* out, void* ws, size_t ws_bytes,
+                        void* stream) {
+  CC_TRY(check_problem(p));
+  CC_TRY(check_kv(p, kv, 1));
+  if (per_head != 0 && per_head != 1) return CC_ERR_ARG;
+  if (!k_h) return CC_ERR_ARG;
+  if (out) {
+    CC_TRY(check_kv(p, out, kv->n_layers));
+    if (out->layout != kv->layout) return CC_ERR_ARG;
+  }
+  const int es = esize(p->dtype);
+  const int row_bytes = p->head_dim * es;
+  if (row_bytes % 16 != 0 || !is_pow2(row_bytes / 16) || row_bytes / 16 > 256)
+    return CC_ERR_UNSUPPORTED;
+  const int hkv = p->n_heads_kv;
+  const int n_lists = p->n_seqs * (per_head ? hkv : 1);
+  CompactPlan plan;
+  plan.lists.resize(n_lists);
+  int64_t off = 0;
+  for (int b = 0; b < p->n_seqs; ++b) {
+    const int n = p->cu_seqlens_h[b + 1] - p->cu_seqlens_h[b];
+    for (int h = 0; h < (per_head ? hkv : 1); ++h) {
+      const int li = per_head ? b * hkv + h : b;
+      const int k = k_h[li];
+      if (k < 0 || k > n) return CC_ERR_SHAPE;
+      plan.lists[li].keep_off = off;
+      plan.lists[li].k = k;
+      plan.lists[li].pad = 0;
+      off += k;
+      plan.max_k = std::max(plan.max_k, k);
+    }
+  }
+  if (off > 0 && !keep_idx) return CC_ERR_ARG;
+  plan.seq_list.resize(p->n_seqs);
+  for (int b = 0; b < p->n_seqs; ++b) plan.seq_list[b] = per_head ? b * hkv : b;
+  const int L = kv->n_layers;
+  for (int b = 0; b < p->n_seqs; ++b)
+    for (int l = 0; l < L; ++l)
+      for (int h = 0; h < hkv; ++h) {
+        const int li = per_head ? b * hkv + h : b;
+        if (plan.lists[li].k == 0) continue;
+        plan.planes.push_back(CompactPlane{b, l, h, li});
+      }
+  std::stable_sort(plan.planes.begin(), plan.planes.end(),
+                   [&](const CompactPlane& a, const CompactPlane& c) {
+                     return plan.lists[a.list].k > plan.lists[c.list].k;
+                   });
+  plan.off_lists = 0;
+  plan.off_planes = align_up(plan.lists.size() * sizeof(CompactList));
+  plan.off_seq = plan.off_planes + align_up(size_t(p->n_seqs) * L * hkv * sizeof(CompactPlane));
+  plan.total = plan.off_seq + align_up(size_t(p->n_seqs) * sizeof(int32_t));
+  if (plan.total != compact_ws_bytes_for(p, per_head, L)) return CC_ERR_ARG;
+  CC_TRY(check_ws(ws, ws_bytes, plan.total));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  CC_HIP(hipMemcpyAsync(at(ws, plan.off_lists), plan.lists.data(),
+                        plan.lists.size() * sizeof(CompactList), hipMemcpyHostToDevice, s));
+  if (!plan.planes.empty())
+    CC_HIP(hipMemcpyAsync(at(ws, plan.off_planes), plan.planes.data(),
+                          plan.planes.size() * sizeof(CompactPlane), hipMemcpyHostToDevice, s));
+  CC_HIP(hipMemcpyAsync(at(ws, plan.off_seq), plan.seq_list.data(),
+                        plan.seq_list.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  CompactLaunch c;
+  const cc_kv* dst = out ? out : kv;
+  c.src[0] = make_view(kv, kv->k, es);
+  c.src[1] = make_view(kv, kv->v, es);
+  c.dst[0] = make_view(dst, dst->k, es);
+  c.dst[1] = make_view(dst, dst->v, es);
+  c.paged = kv->layout == CC_KV_PAGED;
+  c.row_bytes = row_bytes;
+  c.keep = keep_idx;
+  c.lists_d = reinterpret_cast<const CompactList*>(at(ws, plan.off_lists));
+  c.planes_d = reinterpret_cast<const CompactPlane*>(at(ws, plan.off_planes));
+  c.n_planes = int(plan.planes.size());
+  c.max_k = plan.max_k;
+  c.in_place = out == nullptr;
+  c.ids[0] = token_ids;
+  c.ids[1] = pos_ids;
+  c.cu_d = p->cu_seqlens_d;
+  c.seq_list_d = reinterpret_cast<const int32_t*>(at(ws, plan.off_seq));
+  c.n_seqs = p->n_seqs;
+  CC_HIP(launch_compact(c, s));
+  return CC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,422 @@
+// Dense contractions of the scoring pass on CDNA4 MFMA.
+//
+//   y = x W^T          the layer's output projection of the fast variant (Sec. 3.1)
+//   LM head + LSE      z = W_lm u for every cached entry, reduced on the fly to a
+//                      per-(entry, vocabulary tile) pair (max z, sum exp(z - max)) and
+//                      the target logit z[x_i]; a combine kernel turns these into
+//                      logsumexp(z) - z[x_i] (Eq. (5) read as -log P).  The [N][V] logits
+//                      never leave registers.
+//
+// bf16 kernel: C[m][n] = sum_k A[m][k] B[n][k] with both operands K-contiguous, a 256x256
+// workgroup tile, 4 waves each owning a 128x128 sub-tile as 4x4 blocks of the 32x32x16
+// bf16 MFMA (fp32 accumulate), K staged 64 at a time through double-buffered LDS with a
+// padded row stride (144 B) so the 16-byte fragment reads of 8 consecutive rows hit
+// distinct banks.  For the LM head the vocabulary is the MFMA row (M) dimension, so each
+// lane holds 64 logits of one entry and the reduction over the vocabulary is mostly
+// in-lane.  Tiles are rasterised entry-tile-fastest so consecutive workgroups share one
+// LM-head tile.
+// fp32 kernel: a plain LDS-tiled FMA GEMM with the same two epilogues.
+#include "cc_internal.h"
+
+namespace cc {
+namespace {
+
+constexpr int GBM = 256, GBN = 256, GBK = 64;
+constexpr int WGM = 2, WGN = 2, GNT = WGM * WGN * 64;
+constexpr int GTM = GBM / WGM, GTN = GBN / WGN;      // 128 x 128 per wave
+constexpr int GMB = GTM / 32, GNB = GTN / 32;        // 4 x 4 MFMA blocks
+constexpr int GLS = GBK + 8;                         // LDS row stride (elements)
+
+struct GemmArgs {
+  const u16* A;
+  const u16* B;
+  int M, N, K;
+  int64_t lda, ldb;
+  int tiles_n;
+};
+
+__device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<const uint4*>(p); }
+
+struct EpiStore {
+  u16* out;
+  int64_t ldo;
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    (void)tm;
+    (void)lds;
+    const int hi = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int n = n0w + nb * 32 + col;
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+          if (m < g.M) out[int64_t(m) * ldo + n] = f2bf(acc[mb][nb][e]);
+        }
+      }
+  }
+};
+
+// M = vocabulary, N = cached entries.  Writes partial[tm * N + n] = (max, sumexp) over
+// the workgroup's 256 vocabulary rows, and target[n] when ids[n] falls in them.
+struct EpiLse {
+  float2* partial;
+  float* target;
+  const int32_t* ids;
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    const int hi = lane >> 5, col = lane & 31;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
+    __syncthreads();   // LDS tiles are no longer read
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) {
+      const int n = n0w + nb * 32 + col;
+      const int id = n < g.N ? ids[n] : -1;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+          const float z = acc[mb][nb][e];
+          if (m < g.M) mx = fmaxf(mx, z);
+          if (m == id) target[n] = z;
+        }
+      const float mc = mx * kLog2e;
+      float sm = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+          if (m < g.M) sm += exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc));
+        }
+      // combine the two lane halves (rows 4*hi..)
+      const float mx2 = __shfl_xor(mx, 32);
+      const float sm2 = __shfl_xor(sm, 32);
+      const float M = fmaxf(mx, mx2);
+      float S = 0.f;
+      if (M != -INFINITY) S = sm * exp2f((mx - M) * kLog2e) + sm2 * exp2f((mx2 - M) * kLog2e);
+      if (hi == 0) red[wm * GBN + wn * GTN + nb * 32 + col] = make_float2(M, S);
+    }
+    __syncthreads();
+    // waves of row wm == 0 combine across the WGM row groups and write out
+    if (wm == 0 && hi == 0) {
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int c = wn * GTN + nb * 32 + col;
+        const int n = n0w + nb * 32 + col;
+        float M = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < WGM; ++r) M = fmaxf(M, red[r * GBN + c].x);
+        float S = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+          for (int r = 0; r < WGM; ++r) {
+            const float2 p = red[r * GBN + c];
+            S += p.y * exp2f((p.x - M) * kLog2e);
+          }
+        }
+        if (n < g.N) partial[int64_t(tm) * g.N + n] = make_float2(M, S);
+      }
+    }
+  }
+};
+
+template <class Epi>
+__global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
+  __shared__ __attribute__((aligned(16))) u16 lds[2 * (GBM + GBN) * GLS];
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  const int m0 = tm * GBM, n0 = tn * GBN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int hi = lane >> 5, col = lane & 31;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  constexpr int RA = GBM * 8 / GNT, RB = GBN * 8 / GNT, RSTEP = GNT / 8;
+  const int lc = tid & 7, lr = tid >> 3;
+  uint4 ra[RA], rbv[RB];
+
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < RA; ++i) {
+      const int m = m0 + lr + RSTEP * i;
+      ra[i] = m < g.M ? ld16(g.A + int64_t(m) * g.lda + k0 + lc * 8) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int n = n0 + lr + RSTEP * i;
+      rbv[i] = n < g.N ? ld16(g.B + int64_t(n) * g.ldb + k0 + lc * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store = [&](int buf) {
+    u16* As = lds + buf * (GBM + GBN) * GLS;
+    u16* Bs = As + GBM * GLS;
+#pragma unroll
+    for (int i = 0; i < RA; ++i)
+      *reinterpret_cast<uint4*>(As + (lr + RSTEP * i) * GLS + lc * 8) = ra[i];
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+      *reinterpret_cast<uint4*>(Bs + (lr + RSTEP * i) * GLS + lc * 8) = rbv[i];
+  };
+
+  f32x16 acc[GMB][GNB];
+#pragma unroll
+  for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = f32x16{};
+
+  const int nk = g.K / GBK;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) load((kt + 1) * GBK);
+    const u16* As = lds + buf * (GBM + GBN) * GLS;
+    const u16* Bs = As + GBM * GLS;
+#pragma unroll
+    for (int ks = 0; ks < GBK / 16; ++ks) {
+      bf16x8 af[GMB], bfr[GNB];
+#pragma unroll
+      for (int mb = 0; mb < GMB; ++mb)
+        af[mb] = as_bf16x8(ld16(As + (wm * GTM + mb * 32 + col) * GLS + ks * 16 + hi * 8));
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb)
+        bfr[nb] = as_bf16x8(ld16(Bs + (wn * GTN + nb * 32 + col) * GLS + ks * 16 + hi * 8));
+#pragma unroll
+      for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = mfma32(af[mb], bfr[nb], acc[mb][nb]);
+    }
+    if (more) store(buf ^ 1);
+    __syncthreads();
+  }
+  epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds);
+}
+
+// ------------------------------------------------------------------ fp32 path
+
+constexpr int FT = 64, FK = 16;
+
+struct GemmArgsF {
+  const float* A;
+  const float* B;
+  int M, N, K;
+  int64_t lda, ldb;
+  int tiles_n;
+};
+
+struct EpiStoreF {
+  float* out;
+  int64_t ldo;
+  __device__ void operator()(const float (&c)[4][4], const GemmArgsF& g, int tm, int m0, int n0,
+                             float* lds) const {
+    (void)tm;
+    (void)lds;
+    const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+        if (m < g.M && n < g.N) out[int64_t(m) * ldo + n] = c[i][j];
+      }
+  }
+};
+
+struct EpiLseF {
+  float2* partial;
+  float* target;
+  const int32_t* ids;
+  __device__ void operator()(const float (&c)[4][4], const GemmArgsF& g, int tm, int m0, int n0,
+                             float* lds) const {
+    const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+    float* T = lds;   // [FT][FT + 1], T[m][n]
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) T[(ty * 4 + i) * (FT + 1) + tx * 4 + j] = c[i][j];
+    __syncthreads();
+    if (threadIdx.x < FT) {
+      const int nl = threadIdx.x, n = n0 + nl;
+      if (n < g.N) {
+        const int id = ids[n];
+        float mx = -INFINITY;
+        for (int ml = 0; ml < FT && m0 + ml < g.M; ++ml) {
+          const float z = T[ml * (FT + 1) + nl];
+          mx = fmaxf(mx, z);
+          if (m0 + ml == id) target[n] = z;
+        }
+        float s = 0.f;
+        for (int ml = 0; ml < FT && m0 + ml < g.M; ++ml) s += expf(T[ml * (FT + 1) + nl] - mx);
+        partial[int64_t(tm) * g.N + n] = make_float2(mx, s);
+      }
+    }
+  }
+};
+
+template <class Epi>
+__global__ __launch_bounds__(256) void gemm_tn_f32(GemmArgsF g, Epi epi) {
+  __shared__ float lds[FT * (FT + 1)];
+  float* As = lds;                 // [FK][FT + 4]
+  float* Bs = lds + FK * (FT + 4); // [FK][FT + 4]
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  const int m0 = tm * FT, n0 = tn * FT;
+  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  float c[4][4] = {};
+  for (int k0 = 0; k0 < g.K; k0 += FK) {
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < FT * FK; idx += 256) {
+      const int r = idx / FK, kk = idx % FK;
+      const int m = m0 + r, n = n0 + r, k = k0 + kk;
+      As[kk * (FT + 4) + r] = (m < g.M && k < g.K) ? g.A[int64_t(m) * g.lda + k] : 0.f;
+      Bs[kk * (FT + 4) + r] = (n < g.N && k < g.K) ? g.B[int64_t(n) * g.ldb + k] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < FK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = As[kk * (FT + 4) + ty * 4 + i];
+        b[i] = Bs[kk * (FT + 4) + tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) c[i][j] = fmaf(a[i], b[j], c[i][j]);
+    }
+  }
+  epi(c, g, tm, m0, n0, lds);
+}
+
+// ------------------------------------------------------------------ LSE combine
+
+// One workgroup of 4 waves per 64 entries: lane = entry (coalesced reads of the
+// [tile][N] partials), the waves split the vocabulary tiles, then combine in LDS.
+__global__ __launch_bounds__(256) void lse_combine(const float2* partial, int n_tiles,
+                                                   const float* target, const int32_t* cu,
+                                                   int n_seqs, int n_frozen, int N,
+                                                   float* scores, float* lse_out) {
+  __shared__ float2 red[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + lane;
+  float M = -INFINITY, S = 0.f;
+  if (n < N) {
+    for (int t = wave; t < n_tiles; t += 4) {
+      const float2 p = partial[int64_t(t) * N + n];
+      if (p.x == -INFINITY) continue;
+      if (p.x > M) {
+        S = S * expf(M - p.x) + p.y;
+        M = p.x;
+      } else {
+        S += p.y * expf(p.x - M);
+      }
+    }
+  }
+  red[wave][lane] = make_float2(M, S);
+  __syncthreads();
+  if (wave == 0 && n < N) {
+    float Mt = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) Mt = fmaxf(Mt, red[w][lane].x);
+    float St = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (red[w][lane].x != -INFINITY) St += red[w][lane].y * expf(red[w][lane].x - Mt);
+    const float lse = Mt + logf(St);
+    // sequence of entry n: the last b with cu[b] <= n
+    int lo = 0, hi = n_seqs - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (cu[mid] <= n) lo = mid; else hi = mid - 1;
+    }
+    const bool last = n == cu[lo + 1] - 1;
+    const bool frozen = n - cu[lo] < n_frozen;
+    scores[n] = (last || frozen) ? INFINITY : lse - target[n];
+    if (lse_out) lse_out[n] = lse;
+  }
+}
+
+}  // namespace
+
+int lmhead_vocab_tile(int dtype) { return dtype == CC_BF16 ? GBM : FT; }
+
+hipError_t launch_linear(int dtype, const void* x, const void* w, void* y, int M, int N, int K,
+                         hipStream_t s) {
+  if (M == 0 || N == 0) return hipSuccess;
+  if (dtype == CC_BF16) {
+    GemmArgs g;
+    g.A = static_cast<const u16*>(x);
+    g.B = static_cast<const u16*>(w);
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.lda = K;
+    g.ldb = K;
+    g.tiles_n = (N + GBN - 1) / GBN;
+    const int tiles = ((M + GBM - 1) / GBM) * g.tiles_n;
+    EpiStore e{static_cast<u16*>(y), N};
+    hipLaunchKernelGGL(gemm_tn_bf16<EpiStore>, dim3(tiles), dim3(GNT), 0, s, g, e);
+    return hipGetLastError();
+  }
+  GemmArgsF g;
+  g.A = static_cast<const float*>(x);
+  g.B = static_cast<const float*>(w);
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = K;
+  g.ldb = K;
+  g.tiles_n = (N + FT - 1) / FT;
+  const int tiles = ((M + FT - 1) / FT) * g.tiles_n;
+  EpiStoreF e{static_cast<float*>(y), N};
+  hipLaunchKernelGGL(gemm_tn_f32<EpiStoreF>, dim3(tiles), dim3(256), 0, s, g, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
+  if (a.N == 0) return hipSuccess;
+  int n_vt;
+  if (a.dtype == CC_BF16) {
+    GemmArgs g;
+    g.A = static_cast<const u16*>(a.w_lm);
+    g.B = static_cast<const u16*>(a.u);
+    g.M = a.V;
+    g.N = a.N;
+    g.K = a.D;
+    g.lda = a.D;
+    g.ldb = a.D;
+    g.tiles_n = (a.N + GBN - 1) / GBN;
+    n_vt = (a.V + GBM - 1) / GBM;
+    EpiLse e{a.partial, a.target, a.ids};
+    hipLaunchKernelGGL(gemm_tn_bf16<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
+  } else {
+    GemmArgsF g;
+    g.A = static_cast<const float*>(a.w_lm);
+    g.B = static_cast<const float*>(a.u);
+    g.M = a.V;
+    g.N = a.N;
+    g.K = a.D;
+    g.lda = a.D;
+    g.ldb = a.D;
+    g.tiles_n = (a.N + FT - 1) / FT;
+    n_vt = (a.V + FT - 1) / FT;
+    EpiLseF e{a.partial, a.target, a.ids};
+    hipLaunchKernelGGL(gemm_tn_f32<EpiLseF>, dim3(n_vt * g.tiles_n), dim3(256), 0, s, g, e);
+  }
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(lse_combine, dim3((a.N + 63) / 64), dim3(256), 0, s, a.partial, n_vt,
+                     a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores, a.lse);
+  return hipGetLastError();
+}
+
+}  // namespace cc

@@ -1,0 +1,124 @@
+"""Host-side checks of the C ABI: the library loads and exports every entry point the
+header declares, the ctypes structures match the C layout, and argument validation
+rejects bad problems before anything touches a GPU (workspace queries are host-only)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cc.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(cc_\w+)\s*\(", txt, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2607_27600_amd import cc
+    names = _declared()
+    assert len(names) >= 13
+    out = subprocess.run(["nm", "-D", "--defined-only", cc.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (cc_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+    assert set(names) == set(cc.EXPORTED)
+    assert cc.cc_version().startswith("libcc gfx950")
+
+
+def test_struct_layouts_match_header(tmp_path):
+    from paper_2607_27600_amd import cc
+    prog = tmp_path / "layout.c"
+    fields = {
+        "cc_kv": [f[0] for f in cc.c_kv._fields_],
+        "cc_problem": [f[0] for f in cc.c_problem._fields_],
+        "cc_inputs": [f[0] for f in cc.c_inputs._fields_],
+        "cc_layer_weights": [f[0] for f in cc.c_layer_weights._fields_],
+    }
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cc.h"', "int main(void){"]
+    for s, fs in fields.items():
+        lines.append(f'printf("{s} %zu\\n", sizeof({s}));')
+        for f in fs:
+            lines.append(f'printf("{s}.{f} %zu\\n", offsetof({s}, {f}));')
+    lines.append("return 0;}")
+    prog.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(prog), "-o", str(exe)],
+                   check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                 check=True).stdout.splitlines())
+    classes = {"cc_kv": cc.c_kv, "cc_problem": cc.c_problem, "cc_inputs": cc.c_inputs,
+               "cc_layer_weights": cc.c_layer_weights}
+    for s, cls in classes.items():
+        assert int(got[s]) == ctypes.sizeof(cls), s
+        for f in fields[s]:
+            assert int(got[f"{s}.{f}"]) == getattr(cls, f).offset, f"{s}.{f}"
+
+
+def _prob(**kw):
+    from paper_2607_27600_amd import cc
+    cu = (ctypes.c_int32 * 3)(0, 100, 250)
+    p = cc.c_problem()
+    p.dtype, p.mode, p.diag, p.n_seqs = cc.CC_BF16, cc.CC_MODE_LAST_LAYER, cc.CC_DIAG_STRICT, 2
+    p.cu_seqlens_h = ctypes.cast(cu, ctypes.POINTER(ctypes.c_int32))
+    p.cu_seqlens_d = 0x1000          # never dereferenced by a workspace query
+    p.n_heads_q, p.n_heads_kv, p.head_dim, p.hidden, p.vocab = 32, 8, 128, 4096, 128256
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p, cu
+
+
+def test_workspace_queries_and_validation():
+    from paper_2607_27600_amd import cc
+    lib = cc._lib
+    n = ctypes.c_size_t(0)
+    p, _keep = _prob()
+    assert lib.cc_score_workspace(ctypes.byref(p), ctypes.byref(n)) == cc.CC_OK
+    N = 250
+    assert n.value >= N * 32 * 128 * 2 + N * 4096 * 2 + 501 * N * 8
+    bad = [
+        (dict(n_heads_q=30), cc.CC_ERR_SHAPE),
+        (dict(head_dim=96), cc.CC_ERR_UNSUPPORTED),
+        (dict(hidden=4000), cc.CC_ERR_UNSUPPORTED),
+        (dict(dtype=7), cc.CC_ERR_DTYPE),
+        (dict(diag=3), cc.CC_ERR_ARG),
+        (dict(n_frozen=-1), cc.CC_ERR_ARG),
+        (dict(softmax_scale=float("nan")), cc.CC_ERR_ARG),
+        (dict(cu_seqlens_d=None), cc.CC_ERR_ARG),
+        (dict(mode=cc.CC_MODE_FULL, n_layers=0), cc.CC_ERR_SHAPE),
+    ]
+    for kw, want in bad:
+        q, _k = _prob(**kw)
+        assert lib.cc_score_workspace(ctypes.byref(q), ctypes.byref(n)) == want, kw
+    cu_bad = (ctypes.c_int32 * 3)(0, 100, 50)
+    q, _k = _prob()
+    q.cu_seqlens_h = ctypes.cast(cu_bad, ctypes.POINTER(ctypes.c_int32))
+    assert lib.cc_score_workspace(ctypes.byref(q), ctypes.byref(n)) == cc.CC_ERR_SHAPE
+    assert lib.cc_select_workspace(4, ctypes.byref(n)) == cc.CC_OK and n.value >= 4 * 24
+    assert lib.cc_select_workspace(-1, ctypes.byref(n)) == cc.CC_ERR_ARG
+    assert lib.cc_compact_workspace(ctypes.byref(p), 32, 1, ctypes.byref(n)) == cc.CC_OK
+    assert lib.cc_compact_workspace(ctypes.byref(p), 32, 2, ctypes.byref(n)) == cc.CC_ERR_ARG
+
+
+def test_calls_with_bad_arguments_enqueue_nothing():
+    """Argument errors are reported before any HIP call (no GPU is needed to see them)."""
+    from paper_2607_27600_amd import cc
+    lib = cc._lib
+    p, _keep = _prob()
+    assert lib.cc_score(ctypes.byref(p), None, None, None, 0, None) == cc.CC_ERR_ARG
+    kv = cc.c_kv()
+    assert lib.cc_attention_cc(ctypes.byref(p), None, ctypes.byref(kv), 0, None, None, 0,
+                               None) == cc.CC_ERR_ARG
+    st = (ctypes.c_int64 * 1)(0)
+    ln = (ctypes.c_int32 * 1)(10)
+    kk = (ctypes.c_int32 * 1)(11)                   # k > len
+    assert lib.cc_select_keep(None, 1, st, ln, kk, None, None, 0, None) == cc.CC_ERR_SHAPE
+    dummy = ctypes.c_void_p(0x1000)   # never dereferenced: the shape is rejected first
+    assert lib.cc_linear(cc.CC_BF16, dummy, dummy, dummy, 4, 4, 100, None) == cc.CC_ERR_UNSUPPORTED
+    assert lib.cc_linear(cc.CC_BF16, None, None, None, 4, 4, 64, None) == cc.CC_ERR_ARG
+    assert lib.cc_linear(5, None, None, None, 4, 4, 64, None) == cc.CC_ERR_DTYPE
+    for s in range(7):
+        assert cc.cc_status_str(s)

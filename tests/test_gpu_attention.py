@@ -1,0 +1,102 @@
+"""GPU parity of counter-causal attention (cc_attention_cc) against the oracle.
+
+Sizes span several 64-key tiles and 128-row blocks with ragged tails; GQA groups of
+1, 2, 4 and 7; contiguous and paged caches; both mask diagonals; the full-size
+Llama-3-8B shape on sampled rows.  Tolerance for bf16 outputs: the probabilities enter
+the second product rounded to bf16 and the output is stored in bf16, each a relative
+2^-9 error, so |o - ref| <= 2e-2 + 1e-2 |ref|; fp32 outputs agree within 1e-5."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cc_oracle as O
+from synth import configs as C
+from tests.gpu_util import f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(cfg, diag="strict", rows=None):
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    print(f"[attention] {cfg.name} lens={cfg.seq_lens[:8]} hq={cfg.n_heads_q} hkv={cfg.n_heads_kv} "
+          f"paged={cfg.paged} diag={diag}", flush=True)
+    w = Workload(cfg, cache_layers=1, keep_host=True, with_lm_head=False)
+    p = cc.problem(dtype=cfg.dtype, cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=cfg.n_heads_q,
+                   n_heads_kv=cfg.n_heads_kv, head_dim=cfg.head_dim, hidden=cfg.hidden,
+                   vocab=cfg.vocab, diag=diag)
+    o = torch.full_like(w.q, float("nan"))
+    cc.cc_attention_cc(p, w.q, w.kv, 0, o)
+    torch.cuda.synchronize()
+    got = f64(o)
+    cu = cfg.cu_seqlens
+    N = cfg.n_tokens
+    rows = np.arange(N) if rows is None else np.asarray(rows)
+    ref = np.zeros((len(rows), cfg.n_heads_q, cfg.head_dim))
+    seq = np.searchsorted(cu, rows, side="right") - 1
+    for b in np.unique(seq):
+        sel = np.nonzero(seq == b)[0]
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        ref[sel] = O.attention_cc(w.host["q"][lo:hi], w.host["k"][:, lo:hi], w.host["v"][:, lo:hi],
+                                  diag, rows=rows[sel] - lo)
+    return got[rows], ref, rows
+
+
+def _check(got, ref, dtype):
+    assert np.all(np.isfinite(got))
+    if dtype == "bf16":
+        np.testing.assert_allclose(got, ref, rtol=1e-2, atol=2e-2)
+    else:
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-5)
+
+
+def test_c1_fp32_all_rows():
+    got, ref, _ = _run(C.C1)
+    _check(got, ref, "f32")
+    assert np.all(got[-1] == 0)
+
+
+@pytest.mark.parametrize("diag", ["strict", "inclusive"])
+def test_bf16_single_sequence_ragged_tail(diag):
+    cfg = C.shrink(C.C2, seq_lens=(300,), cache_layers=1)
+    got, ref, _ = _run(cfg, diag)
+    _check(got, ref, "bf16")
+    if diag == "strict":
+        assert np.all(got[-1] == 0)
+        # row n-2 attends only to the last entry: its output is that value row, rounded
+        np.testing.assert_allclose(got[-2], ref[-2], rtol=0, atol=1e-2)
+
+
+def test_bf16_ragged_batch_gqa7():
+    cfg = C.shrink(C.C5, seq_lens=(1, 2, 63, 64, 65, 200), paged=False, cache_layers=1,
+                   keep=(1, 1, 1, 1, 1, 1))
+    got, ref, _ = _run(cfg)
+    _check(got, ref, "bf16")
+
+
+def test_bf16_paged_pool():
+    cfg = C.shrink(C.C5, seq_lens=(17, 100, 260, 16), cache_layers=1, keep=(1, 1, 1, 1))
+    got, ref, _ = _run(cfg)
+    _check(got, ref, "bf16")
+
+
+def test_bf16_mha_and_gqa2():
+    for hq, hkv in ((4, 4), (8, 4)):
+        cfg = C.shrink(C.C2, seq_lens=(130, 70), n_heads_q=hq, n_heads_kv=hkv, cache_layers=1,
+                       keep=(1, 1))
+        got, ref, _ = _run(cfg)
+        _check(got, ref, "bf16")
+
+
+@pytest.mark.slow
+def test_c2_full_size_sampled_rows():
+    rows = C.sample_rows(C.C2, count=96)
+    got, ref, _ = _run(C.C2, rows=rows)
+    _check(got, ref, "bf16")
+
+
+@pytest.mark.slow
+def test_c5_full_size_paged_sampled_rows():
+    rows = C.sample_rows(C.C5, count=64)
+    got, ref, _ = _run(C.C5, rows=rows)
+    _check(got, ref, "bf16")

@@ -1,0 +1,124 @@
+"""GPU parity of the scoring pass (cc_linear, cc_lmhead_score, cc_score) against the
+oracle: surprise scores within 2e-2 + 1e-2 |ref| in bf16 and 1e-5 in fp32, +inf entries
+exact (last entry of every sequence, frozen sinks)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cc_oracle as O
+from synth import configs as C
+from synth import gen
+from tests.gpu_util import assert_scores_close, dev, f64
+
+pytestmark = pytest.mark.gpu
+
+
+def test_linear_bf16_tiles_and_tails():
+    from paper_2607_27600_amd import cc
+    print("[linear] bf16 300x4096 @ 520x4096", flush=True)
+    r = np.random.default_rng(0)
+    x = gen.f32_to_bf16_bits(r.standard_normal((300, 4096)).astype(np.float32))
+    w = gen.f32_to_bf16_bits((0.02 * r.standard_normal((520, 4096))).astype(np.float32))
+    y = torch.empty((300, 520), dtype=torch.bfloat16, device="cuda")
+    cc.cc_linear("bf16", dev(x), dev(w), y)
+    torch.cuda.synchronize()
+    ref = O.f64(x) @ O.f64(w).T
+    # fp32 accumulation of 4096 exact products, then one bf16 rounding (2^-9 relative)
+    np.testing.assert_allclose(f64(y), ref, rtol=4e-3, atol=1e-4)
+
+
+def test_linear_f32():
+    from paper_2607_27600_amd import cc
+    r = np.random.default_rng(1)
+    x = r.standard_normal((70, 128)).astype(np.float32)
+    w = r.standard_normal((130, 128)).astype(np.float32)
+    y = torch.empty((70, 130), dtype=torch.float32, device="cuda")
+    cc.cc_linear("f32", dev(x), dev(w), y)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(f64(y), x.astype(np.float64) @ w.astype(np.float64).T, rtol=0,
+                               atol=1e-4)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_lmhead_ragged_vocab_and_rows(dtype):
+    from paper_2607_27600_amd import cc
+    print(f"[lmhead] {dtype}", flush=True)
+    r = np.random.default_rng(2)
+    lens = [5, 1, 294]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    N, D, V = int(cu[-1]), 256, 1000
+    u = r.standard_normal((N, D)).astype(np.float32)
+    w = (0.05 * r.standard_normal((V, D))).astype(np.float32)
+    ids = r.integers(0, V, N).astype(np.int32)
+    if dtype == "bf16":
+        u, w = gen.f32_to_bf16_bits(u), gen.f32_to_bf16_bits(w)
+    p = cc.problem(dtype=dtype, cu_seqlens=cu.tolist(), n_heads_q=1, n_heads_kv=1,
+                   head_dim=128, hidden=D, vocab=V, n_frozen=2)
+    scores = torch.empty(N, dtype=torch.float32, device="cuda")
+    lse = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score(p, dev(u), dev(w), dev(ids), scores, lse)
+    torch.cuda.synchronize()
+    s_ref, lse_ref, _ = O.surprise(O.f64(u), w, ids)
+    s_ref[O.edge_rows(cu, 2)] = np.inf
+    assert_scores_close(scores.cpu().numpy(), s_ref, dtype, "lmhead")
+    tol = 1e-5 if dtype == "f32" else 2e-2
+    np.testing.assert_allclose(lse.cpu().numpy(), lse_ref, rtol=0, atol=tol)
+
+
+def test_lmhead_zero_head_gives_ln_vocab():
+    from paper_2607_27600_amd import cc
+    N, D, V = 100, 128, 128256
+    u = gen.f32_to_bf16_bits(np.random.default_rng(3).standard_normal((N, D)).astype(np.float32))
+    w = torch.zeros((V, D), dtype=torch.bfloat16, device="cuda")
+    ids = torch.arange(N, dtype=torch.int32, device="cuda") * 997
+    p = cc.problem(dtype="bf16", cu_seqlens=[0, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
+                   hidden=D, vocab=V)
+    scores = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score(p, dev(u), w, ids, scores)
+    torch.cuda.synchronize()
+    s = scores.cpu().numpy().astype(np.float64)
+    assert s[-1] == np.inf
+    np.testing.assert_allclose(s[:-1], np.log(V), rtol=0, atol=2e-5)
+
+
+def _score_case(cfg, rows=None):
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    print(f"[score] {cfg.name} lens={cfg.seq_lens[:8]} dtype={cfg.dtype} paged={cfg.paged}",
+          flush=True)
+    w = Workload(cfg, cache_layers=1, keep_host=True)
+    scores = torch.full((cfg.n_tokens,), float("nan"), dtype=torch.float32, device="cuda")
+    cc.cc_score(w.problem, w.inputs(), scores)
+    torch.cuda.synchronize()
+    got = scores.cpu().numpy()
+    h = w.host
+    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                              cfg.cu_seqlens, rows=rows)
+    got = got if rows is None else got[rows]
+    return got, ref
+
+
+def test_score_c1_fp32_all_rows():
+    got, ref = _score_case(C.C1)
+    stats = assert_scores_close(got, ref, "f32", "C1")
+    print("C1", stats)
+
+
+def test_score_bf16_small_all_rows():
+    cfg = C.shrink(C.C2, seq_lens=(300,), hidden=256, vocab=1000, cache_layers=1)
+    got, ref = _score_case(cfg)
+    print(assert_scores_close(got, ref, "bf16", "bf16-small"))
+
+
+def test_score_bf16_paged_ragged_all_rows():
+    cfg = C.shrink(C.C5, seq_lens=(33, 1, 150, 64), hidden=512, vocab=3000, cache_layers=1,
+                   keep=(1, 1, 1, 1))
+    got, ref = _score_case(cfg)
+    print(assert_scores_close(got, ref, "bf16", "paged-small"))
+
+
+@pytest.mark.slow
+def test_score_c2_full_size_sampled():
+    rows = C.sample_rows(C.C2, count=64)
+    got, ref = _score_case(C.C2, rows=rows)
+    print(assert_scores_close(got, ref, "bf16", "C2"))

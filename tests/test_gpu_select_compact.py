@@ -1,0 +1,152 @@
+"""GPU keep selection and KV compaction: bit-exact against the oracle.
+
+Selection is compared on identical fp32 scores (ties, -0/+0, +/-inf, NaN, ragged
+segments, k = 0 and k = len); compaction is a bit copy compared byte for byte, in place
+and out of place, contiguous and paged, one list per sequence or per KV head."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cc_oracle as O
+from synth import configs as C
+from tests.gpu_util import bf16_host
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_select(scores: np.ndarray, starts, lens, ks):
+    from paper_2607_27600_amd import cc
+    s = torch.from_numpy(scores.astype(np.float32)).cuda()
+    keep = torch.full((max(1, int(sum(ks))),), -7, dtype=torch.int32, device="cuda")
+    cc.cc_select_keep(s, starts, lens, ks, keep)
+    torch.cuda.synchronize()
+    return keep.cpu().numpy()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_select_matches_oracle_with_ties(seed):
+    print(f"[select] seed={seed}", flush=True)
+    r = np.random.default_rng(seed)
+    lens = [1, 2, 7, 1000, 1024, 1025, 5000, 32768]
+    total = sum(lens)
+    pool = np.array([-0.0, 0.0, 1.5, 1.5, 2.0, -3.0, np.inf, -np.inf, np.nan, 11.75],
+                    dtype=np.float32)
+    s = np.where(r.random(total) < 0.5, pool[r.integers(0, len(pool), total)],
+                 np.round(r.standard_normal(total), 2).astype(np.float32)).astype(np.float32)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    for kfrac in (0.0, 0.25, 0.5, 1.0):
+        ks = [int(kfrac * n) for n in lens]
+        got = _gpu_select(s, starts, lens, ks)
+        off = 0
+        for st, n, k in zip(starts, lens, ks):
+            ref = O.select_keep(s[st:st + n], k)
+            np.testing.assert_array_equal(got[off:off + k], ref, err_msg=f"len={n} k={k}")
+            off += k
+
+
+def test_select_overlapping_segments_identical_lists():
+    r = np.random.default_rng(9)
+    s = r.standard_normal(4096).astype(np.float32)
+    s[-1] = np.inf
+    got = _gpu_select(s, [0] * 8, [4096] * 8, [1024] * 8).reshape(8, 1024)
+    ref = O.select_keep(s, 1024)
+    for h in range(8):
+        np.testing.assert_array_equal(got[h], ref)
+
+
+def test_select_all_equal_scores():
+    s = np.full(3000, np.log(128256.0), dtype=np.float32)
+    s[-1] = np.inf
+    got = _gpu_select(s, [0], [3000], [700])
+    np.testing.assert_array_equal(got, np.r_[np.arange(699), 2999])
+
+
+def _contig_cache(L, B, hkv, cap, d, seed, dtype=torch.bfloat16):
+    g = torch.Generator().manual_seed(seed)
+    k = torch.randn((B, L, hkv, cap, d), generator=g).to(dtype).cuda()
+    v = torch.randn((B, L, hkv, cap, d), generator=g).to(dtype).cuda()
+    return k, v
+
+
+@pytest.mark.parametrize("in_place", [True, False])
+@pytest.mark.parametrize("per_head", [0, 1])
+def test_compact_contiguous(in_place, per_head):
+    from paper_2607_27600_amd import cc
+    print(f"[compact] contiguous in_place={in_place} per_head={per_head}", flush=True)
+    L, hkv, d = 3, 4, 128
+    lens = [300, 1, 1000]
+    B, cap = len(lens), max(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    k, v = _contig_cache(L, B, hkv, cap, d, seed=1)
+    k0, v0 = k.clone(), v.clone()
+    r = np.random.default_rng(3)
+    lists, kk = [], []
+    for b, n in enumerate(lens):
+        for h in range(hkv if per_head else 1):
+            kb = max(1, n // 4) if h % 2 == 0 else n // 3
+            kb = min(kb, n)
+            lists.append(np.sort(r.choice(n, kb, replace=False)).astype(np.int32))
+            kk.append(kb)
+    keep = torch.from_numpy(np.concatenate(lists)).cuda()
+    ids = torch.from_numpy(r.integers(0, 1000, cu[-1]).astype(np.int32)).cuda()
+    pos = torch.arange(int(cu[-1]), dtype=torch.int32).cuda()
+    ids0, pos0 = ids.clone(), pos.clone()
+    p = cc.problem(dtype="bf16", cu_seqlens=cu.tolist(), n_heads_q=hkv, n_heads_kv=hkv, head_dim=d,
+                   hidden=128, vocab=1000)
+    strides = dict(n_layers=L, seq_stride=L * hkv * cap * d, layer_stride=hkv * cap * d,
+                   head_stride=cap * d, tok_stride=d)
+    kv = cc.kv_contiguous(k, v, **strides)
+    if in_place:
+        cc.cc_compact_kv(p, kv, keep, kk, per_head, ids, pos)
+        ok, ov = k, v
+    else:
+        ok, ov = torch.zeros_like(k), torch.zeros_like(v)
+        out = cc.kv_contiguous(ok, ov, **strides)
+        cc.cc_compact_kv(p, kv, keep, kk, per_head, ids, pos, out=out)
+    torch.cuda.synchronize()
+    K0, V0 = bf16_host(k0), bf16_host(v0)
+    KO, VO = bf16_host(ok), bf16_host(ov)
+    li = 0
+    for b, n in enumerate(lens):
+        for h in range(hkv):
+            lst = lists[b * hkv + h] if per_head else lists[b]
+            kb = len(lst)
+            for l in range(L):
+                np.testing.assert_array_equal(KO[b, l, h, :kb], O.compact(K0[b, l, h], lst))
+                np.testing.assert_array_equal(VO[b, l, h, :kb], O.compact(V0[b, l, h], lst))
+                if in_place:   # entries past k untouched
+                    np.testing.assert_array_equal(KO[b, l, h, kb:], K0[b, l, h, kb:])
+        first = lists[b * hkv] if per_head else lists[b]
+        lo = cu[b]
+        np.testing.assert_array_equal(ids.cpu().numpy()[lo:lo + len(first)],
+                                      ids0.cpu().numpy()[lo + first])
+        np.testing.assert_array_equal(pos.cpu().numpy()[lo:lo + len(first)], lo + first)
+
+
+def test_compact_paged_in_place_matches_out_of_place():
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.shrink(C.C5, seq_lens=(40, 300, 17), cache_layers=2, keep=(8, 60, 17), vocab=1000,
+                   hidden=256)
+    w = Workload(cfg, cache_layers=2, with_lm_head=False)
+    r = np.random.default_rng(5)
+    lists = [np.sort(r.choice(n, kb, replace=False)).astype(np.int32)
+             for n, kb in zip(cfg.seq_lens, cfg.keep)]
+    keep = torch.from_numpy(np.concatenate(lists)).cuda()
+    k0, v0 = w.k_cache.clone(), w.v_cache.clone()
+    ok, ov = torch.zeros_like(k0), torch.zeros_like(v0)
+    P = cfg.page_size
+    npg, hkv, d = k0.shape[1], cfg.n_heads_kv, cfg.head_dim
+    out = cc.kv_paged(ok, ov, w.block_table, n_layers=2, layer_stride=npg * hkv * P * d,
+                      page_stride=hkv * P * d, head_stride=P * d, tok_stride=d, page_size=P)
+    cc.cc_compact_kv(w.problem, w.kv, keep, list(cfg.keep), 0, out=out)
+    cc.cc_compact_kv(w.problem, w.kv, keep, list(cfg.keep), 0)   # in place
+    torch.cuda.synchronize()
+    bt = w.block_table.cpu().numpy()
+    K0, KI, KO = bf16_host(k0), bf16_host(w.k_cache), bf16_host(ok)
+    for b, lst in enumerate(lists):
+        for j, src in enumerate(lst):
+            for l in range(2):
+                want = K0[l, bt[b, src // P], :, src % P]
+                np.testing.assert_array_equal(KI[l, bt[b, j // P], :, j % P], want)
+                np.testing.assert_array_equal(KO[l, bt[b, j // P], :, j % P], want)
