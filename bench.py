@@ -1,0 +1,212 @@
+"""Benchmark of the counter-causal refresh pass on one MI355X.
+
+One step is one whole refresh of the Llama-3-8B-shaped fast (last-layer) workload:
+counter-causal attention over the last cache layer (n = 4096 cached tokens, 32 query /
+8 KV heads, head_dim 128), the output projection, the LM head (vocab 128256) with the
+fused log-sum-exp and target gather, keep selection of 1024 entries, and compaction of
+the 32-layer KV cache.  Inputs are seeded synthetic data resident in HBM before the
+timed region.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_HBM_GBS = 8000.0
+METRIC = "cached tokens scored/sec per refresh; attention TFLOP/s as % of bf16 MFMA peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="C2")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=256)
+    return ap.parse_args()
+
+
+def cpu_baseline(w, rows_count: int) -> dict:
+    """The oracle (fp64 NumPy) on this host: scores of a seeded row sample, extrapolated by
+    row count, plus full selection and compaction of one cache layer pair."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import cc_oracle as O
+    from synth import configs as C
+
+    cfg = w.cfg
+    h = w.host
+    rows = C.sample_rows(cfg, count=rows_count)
+    t0 = time.perf_counter()
+    s = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                            cfg.cu_seqlens, rows=rows)
+    t_score = (time.perf_counter() - t0) * cfg.n_tokens / len(rows)
+    # selection and compaction run in full on a full score vector (sampled scores, the
+    # rest filled deterministically: selection cost does not depend on values)
+    full = np.zeros(cfg.n_tokens)
+    full[rows] = s
+    t0 = time.perf_counter()
+    keep = O.select_keep(full, cfg.keep[0])
+    t_sel = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    plane = h["k"][0]                                    # one [N][d] plane
+    O.compact(plane, keep)
+    t_plane = time.perf_counter() - t0
+    planes = 2 * w.cache_layers * cfg.n_heads_kv
+    t_compact = t_plane * planes
+    total = t_score + t_sel + t_compact
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": cfg.n_tokens / total, "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"fp64 oracle scores of {len(rows)} of {cfg.n_tokens} rows (first/last "
+                       f"rows of the sequence plus uniform picks), time scaled by row count; "
+                       f"full selection; compaction of one [{cfg.n_tokens}][{cfg.head_dim}] plane "
+                       f"scaled by the {planes} planes of the cache"),
+            "seconds": {"score_extrapolated": t_score, "select": t_sel,
+                        "compact_extrapolated": t_compact}}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the refresh pass is "
+              "built and measured on one MI355X; multi-GPU sharding is a design note only.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    from synth import configs as C
+
+    cfg = C.CONFIGS[args.config]
+    assert cfg.mode == "last_layer" and not cfg.paged and cfg.n_seqs == 1, \
+        "bench.py times the single-sequence fast-path workloads"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    w = Workload(cfg, device=dev, keep_host=not args.no_cpu_baseline)
+    t_gen = time.perf_counter() - t_gen
+    p = w.problem
+    N, Hq, d, D, V = cfg.n_tokens, cfg.n_heads_q, cfg.head_dim, cfg.hidden, cfg.vocab
+    L, hkv = w.cache_layers, cfg.n_heads_kv
+    k_keep = cfg.keep[0]
+    n_lists = hkv if cfg.per_head_select else 1
+
+    # buffers and workspaces (allocated once, outside the timed region)
+    o = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=dev)
+    u = torch.empty((N, D), dtype=torch.bfloat16, device=dev)
+    scores = torch.empty(N, dtype=torch.float32, device=dev)
+    keep = torch.empty(n_lists * k_keep, dtype=torch.int32, device=dev)
+    ws_att = torch.empty(max(1, cc.cc_attention_workspace(p)), dtype=torch.uint8, device=dev)
+    ws_lm = torch.empty(max(1, cc.cc_lmhead_workspace(p)), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(max(1, cc.cc_select_workspace(n_lists)), dtype=torch.uint8, device=dev)
+    ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, int(cfg.per_head_select))),
+                         dtype=torch.uint8, device=dev)
+    out_k = torch.empty_like(w.k_cache)
+    out_v = torch.empty_like(w.v_cache)
+    cap = w.k_cache.shape[3]
+    out_kv = cc.kv_contiguous(out_k, out_v, n_layers=L, seq_stride=L * hkv * cap * d,
+                              layer_stride=hkv * cap * d, head_stride=cap * d, tok_stride=d)
+    seg_start = [0] * n_lists
+    seg_len = [N] * n_lists
+    ks = [k_keep] * n_lists
+    stream = torch.cuda.current_stream()
+    names = ["attention", "wo_proj", "lmhead_lse", "select", "compact"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        cc.cc_attention_cc(p, w.q, w.kv, L - 1, o, ws_att)
+        mark(1)
+        cc.cc_linear("bf16", o.view(N, Hq * d), w.w_o, u)
+        mark(2)
+        cc.cc_lmhead_score(p, u, w.w_lm, w.ids, scores, workspace=ws_lm)
+        mark(3)
+        cc.cc_select_keep(scores, seg_start, seg_len, ks, keep, ws_sel)
+        mark(4)
+        cc.cc_compact_kv(p, w.kv, keep, ks, int(cfg.per_head_select), out=out_kv, workspace=ws_cmp)
+        mark(5)
+
+    # the sub-step chain is the same work as cc_score; check once that they agree
+    ref_scores = torch.empty_like(scores)
+    cc.cc_score(p, w.inputs(), ref_scores)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if not torch.equal(ref_scores, scores) and args.warmup > 0:
+        raise SystemExit("sub-step chain and cc_score disagree")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    part_ms = {n: 0.0 for n in names}
+    for e in evs:
+        for j, n in enumerate(names):
+            part_ms[n] += e[j].elapsed_time(e[j + 1]) / args.steps
+    ms_step = elapsed * 1e3 / args.steps
+
+    att_flop = 2.0 * d * Hq * sum(n * (n - 1) for n in cfg.seq_lens)
+    lm_flop = 2.0 * N * D * V
+    wo_flop = 2.0 * N * D * Hq * d
+    lm_tflops = lm_flop / (part_ms["lmhead_lse"] * 1e-3) / 1e12
+    att_tflops = att_flop / (part_ms["attention"] * 1e-3) / 1e12
+    kept_bytes = 2 * L * hkv * k_keep * d * 2 * (1 if not cfg.per_head_select else 1)
+    compact_gbs = 2 * kept_bytes / (part_ms["compact"] * 1e-3) / 1e9
+
+    res = {
+        "metric": METRIC,
+        "value": N / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "n_cached": N,
+                   "n_heads_q": Hq, "n_heads_kv": hkv, "head_dim": d, "hidden": D, "vocab": V,
+                   "keep": k_keep, "cache_layers": L, "variant": "fast last-layer"},
+        "roofline": {"kernel": "LM head GEMM + fused log-sum-exp (gemm_tn_bf16<EpiLse> + "
+                               "lse_combine)",
+                     "bound": "mfma", "achieved": lm_tflops, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": lm_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flop_per_launch": lm_flop},
+        "attention": {"tflops": att_tflops, "frac_bf16_peak": att_tflops / PEAK_BF16_TFLOPS,
+                      "flop_per_launch": att_flop},
+        "compact": {"gb_s": compact_gbs, "frac_hbm": compact_gbs / PEAK_HBM_GBS,
+                    "bytes_moved": 2 * kept_bytes, "mode": "out of place, 32-layer cache"},
+        "breakdown_ms": part_ms,
+        "wo_proj_tflops": wo_flop / (part_ms["wo_proj"] * 1e-3) / 1e12,
+        "input_generation_s": t_gen,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_rows)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

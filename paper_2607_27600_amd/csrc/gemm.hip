@@ -32,7 +32,7 @@ struct GemmArgs {
   const u16* B;
   int M, N, K;
   int64_t lda, ldb;
-  int tiles_n;
+  int tiles_m, tiles_n;
 };
 
 __device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<const uint4*>(p); }
@@ -73,35 +73,54 @@ struct EpiLse {
     const int wm = wave / WGN, wn = wave % WGN;
     float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
     __syncthreads();   // LDS tiles are no longer read
+    int id[GNB];
+    float mx[GNB], sm[GNB];
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
       const int n = n0w + nb * 32 + col;
-      const int id = n < g.N ? ids[n] : -1;
-      float mx = -INFINITY;
+      id[nb] = n < g.N ? ids[n] : -1;
+      mx[nb] = -INFINITY;
+      sm[nb] = 0.f;
+    }
+    // pass 1: per-entry max over this lane's vocabulary rows, and the target logit
 #pragma unroll
-      for (int mb = 0; mb < GMB; ++mb)
+    for (int mb = 0; mb < GMB; ++mb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+        const bool mv = m < g.M;
+#pragma unroll
+        for (int nb = 0; nb < GNB; ++nb) {
           const float z = acc[mb][nb][e];
-          if (m < g.M) mx = fmaxf(mx, z);
-          if (m == id) target[n] = z;
+          mx[nb] = mv ? fmaxf(mx[nb], z) : mx[nb];
+          if (m == id[nb]) target[n0w + nb * 32 + col] = z;
         }
-      const float mc = mx * kLog2e;
-      float sm = 0.f;
+      }
+    // pass 2: sum of exp(z - max)
+    float mc[GNB];
 #pragma unroll
-      for (int mb = 0; mb < GMB; ++mb)
+    for (int nb = 0; nb < GNB; ++nb) mc[nb] = mx[nb] * kLog2e;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-          if (m < g.M) sm += exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc));
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+        const bool mv = m < g.M;
+#pragma unroll
+        for (int nb = 0; nb < GNB; ++nb) {
+          const float t = exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
+          sm[nb] += mv ? t : 0.f;
         }
+      }
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) {
       // combine the two lane halves (rows 4*hi..)
-      const float mx2 = __shfl_xor(mx, 32);
-      const float sm2 = __shfl_xor(sm, 32);
-      const float M = fmaxf(mx, mx2);
+      const float mx2 = __shfl_xor(mx[nb], 32);
+      const float sm2 = __shfl_xor(sm[nb], 32);
+      const float M = fmaxf(mx[nb], mx2);
       float S = 0.f;
-      if (M != -INFINITY) S = sm * exp2f((mx - M) * kLog2e) + sm2 * exp2f((mx2 - M) * kLog2e);
+      if (M != -INFINITY)
+        S = sm[nb] * exp2f((mx[nb] - M) * kLog2e) + sm2 * exp2f((mx2 - M) * kLog2e);
       if (hi == 0) red[wm * GBN + wn * GTN + nb * 32 + col] = make_float2(M, S);
     }
     __syncthreads();
@@ -128,10 +147,38 @@ struct EpiLse {
   }
 };
 
+// Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8 XCDs (each
+// with its own L2), so consecutive logical tiles are first given to one XCD, then the
+// logical order walks groups of GROUP_M tile rows with the row index fastest: the ~32
+// workgroups an XCD runs at once cover a 4 x 8 block of tiles and share their A and B
+// k-slices in that XCD's L2.
+constexpr int GROUP_M = 4;
+
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int T = tiles_m * tiles_n;
+  const int per = T / 8, rem = T % 8;
+  const int x = bid % 8, j = bid / 8;
+  const int L = x * per + min(x, rem) + j;
+  const int group = L / (GROUP_M * tiles_n);
+  const int first = group * GROUP_M;
+  const int gsize = min(GROUP_M, tiles_m - first);
+  const int within = L - group * GROUP_M * tiles_n;
+  tm = first + within % gsize;
+  tn = within / gsize;
+}
+
+// Scheduling hints: interleave MFMAs with LDS reads / writes / global loads so the matrix
+// pipe stays busy while the wave issues its memory traffic.
+#define SCHED_MFMA 0x008
+#define SCHED_VMEM_READ 0x020
+#define SCHED_DS_READ 0x100
+#define SCHED_DS_WRITE 0x200
+
 template <class Epi>
 __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   __shared__ __attribute__((aligned(16))) u16 lds[2 * (GBM + GBN) * GLS];
-  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  int tm, tn;
+  tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
   const int m0 = tm * GBM, n0 = tn * GBN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int hi = lane >> 5, col = lane & 31;
@@ -139,21 +186,25 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
 
   constexpr int RA = GBM * 8 / GNT, RB = GBN * 8 / GNT, RSTEP = GNT / 8;
   const int lc = tid & 7, lr = tid >> 3;
+  // Rows past the matrix edge are clamped to the last row: their products land in output
+  // rows/columns the epilogues discard, so no zero fill (and no branch) is needed.
+  const u16* pa[RA];
+  const u16* pb[RB];
+#pragma unroll
+  for (int i = 0; i < RA; ++i)
+    pa[i] = g.A + int64_t(min(m0 + lr + RSTEP * i, g.M - 1)) * g.lda + lc * 8;
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+    pb[i] = g.B + int64_t(min(n0 + lr + RSTEP * i, g.N - 1)) * g.ldb + lc * 8;
   uint4 ra[RA], rbv[RB];
 
-  auto load = [&](int k0) {
+  auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < RA; ++i) {
-      const int m = m0 + lr + RSTEP * i;
-      ra[i] = m < g.M ? ld16(g.A + int64_t(m) * g.lda + k0 + lc * 8) : make_uint4(0, 0, 0, 0);
-    }
+    for (int i = 0; i < RA; ++i) ra[i] = ld16(pa[i] + k0);
 #pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      const int n = n0 + lr + RSTEP * i;
-      rbv[i] = n < g.N ? ld16(g.B + int64_t(n) * g.ldb + k0 + lc * 8) : make_uint4(0, 0, 0, 0);
-    }
+    for (int i = 0; i < RB; ++i) rbv[i] = ld16(pb[i] + k0);
   };
-  auto store = [&](int buf) {
+  auto lstore = [&](int buf) {
     u16* As = lds + buf * (GBM + GBN) * GLS;
     u16* Bs = As + GBM * GLS;
 #pragma unroll
@@ -163,40 +214,93 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     for (int i = 0; i < RB; ++i)
       *reinterpret_cast<uint4*>(Bs + (lr + RSTEP * i) * GLS + lc * 8) = rbv[i];
   };
+  auto fread = [&](int buf, int ks, bf16x8 (&fa)[GMB], bf16x8 (&fb)[GNB]) {
+    const u16* As = lds + buf * (GBM + GBN) * GLS;
+    const u16* Bs = As + GBM * GLS;
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+      fa[mb] = as_bf16x8(ld16(As + (wm * GTM + mb * 32 + col) * GLS + ks * 16 + hi * 8));
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb)
+      fb[nb] = as_bf16x8(ld16(Bs + (wn * GTN + nb * 32 + col) * GLS + ks * 16 + hi * 8));
+  };
 
   f32x16 acc[GMB][GNB];
 #pragma unroll
   for (int mb = 0; mb < GMB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = f32x16{};
+  auto mfmas = [&](const bf16x8 (&fa)[GMB], const bf16x8 (&fb)[GNB]) {
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = mfma32(fa[mb], fb[nb], acc[mb][nb]);
+  };
 
   const int nk = g.K / GBK;
-  load(0);
-  store(0);
+  bf16x8 fa0[GMB], fb0[GNB], fa1[GMB], fb1[GNB];
+  gload(0);
+  lstore(0);
   __syncthreads();
+  fread(0, 0, fa0, fb0);
+  if (nk > 1) gload(GBK);
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) load((kt + 1) * GBK);
-    const u16* As = lds + buf * (GBM + GBN) * GLS;
-    const u16* Bs = As + GBM * GLS;
+    // k-step 0: read step-1 fragments while the step-0 MFMAs run
+    __builtin_amdgcn_sched_barrier(0);
+    fread(buf, 1, fa1, fb1);
+    mfmas(fa0, fb0);
 #pragma unroll
-    for (int ks = 0; ks < GBK / 16; ++ks) {
-      bf16x8 af[GMB], bfr[GNB];
-#pragma unroll
-      for (int mb = 0; mb < GMB; ++mb)
-        af[mb] = as_bf16x8(ld16(As + (wm * GTM + mb * 32 + col) * GLS + ks * 16 + hi * 8));
-#pragma unroll
-      for (int nb = 0; nb < GNB; ++nb)
-        bfr[nb] = as_bf16x8(ld16(Bs + (wn * GTN + nb * 32 + col) * GLS + ks * 16 + hi * 8));
-#pragma unroll
-      for (int mb = 0; mb < GMB; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = mfma32(af[mb], bfr[nb], acc[mb][nb]);
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
     }
-    if (more) store(buf ^ 1);
+    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // k-step 1
+    fread(buf, 2, fa0, fb0);
+    mfmas(fa1, fb1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // k-step 2, then the next tile goes from registers to the other LDS buffer
+    fread(buf, 3, fa1, fb1);
+    mfmas(fa0, fb0);
+    lstore(buf ^ 1);   // on the last tile this fills a buffer nobody reads
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_WRITE, 2, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
+    // k-step 3: fragments of the next tile's step 0 and the global loads two tiles ahead
+    // are issued between the MFMAs
+    fread(buf ^ 1, 0, fa0, fb0);
+    gload(min(kt + 2, nk - 1) * GBK);   // past the end: a harmless reload of the last tile
+    mfmas(fa1, fb1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_VMEM_READ, 2, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
+  __syncthreads();
   epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds);
 }
 
@@ -299,38 +403,41 @@ __global__ __launch_bounds__(256) void gemm_tn_f32(GemmArgsF g, Epi epi) {
 
 // ------------------------------------------------------------------ LSE combine
 
-// One workgroup of 4 waves per 64 entries: lane = entry (coalesced reads of the
-// [tile][N] partials), the waves split the vocabulary tiles, then combine in LDS.
-__global__ __launch_bounds__(256) void lse_combine(const float2* partial, int n_tiles,
-                                                   const float* target, const int32_t* cu,
-                                                   int n_seqs, int n_frozen, int N,
-                                                   float* scores, float* lse_out) {
-  __shared__ float2 red[4][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = blockIdx.x * 64 + lane;
+// One workgroup per 16 entries: thread (group gi, entry e) folds the vocabulary tiles
+// gi, gi+16, ... of entry e (16 consecutive entries read 128 contiguous bytes of a tile's
+// row of partials), then the 16 groups are folded in LDS.
+constexpr int CMB_E = 16, CMB_G = 16;
+
+__device__ __forceinline__ void lse_fold(float& M, float& S, float m, float s) {
+  if (m == -INFINITY) return;
+  if (m > M) {
+    S = S * expf(M - m) + s;
+    M = m;
+  } else {
+    S += s * expf(m - M);
+  }
+}
+
+__global__ __launch_bounds__(CMB_E * CMB_G) void lse_combine(const float2* partial, int n_tiles,
+                                                            const float* target, const int32_t* cu,
+                                                            int n_seqs, int n_frozen, int N,
+                                                            float* scores, float* lse_out) {
+  __shared__ float2 red[CMB_G][CMB_E];
+  const int e = threadIdx.x % CMB_E, gi = threadIdx.x / CMB_E;
+  const int n = blockIdx.x * CMB_E + e;
   float M = -INFINITY, S = 0.f;
   if (n < N) {
-    for (int t = wave; t < n_tiles; t += 4) {
+    for (int t = gi; t < n_tiles; t += CMB_G) {
       const float2 p = partial[int64_t(t) * N + n];
-      if (p.x == -INFINITY) continue;
-      if (p.x > M) {
-        S = S * expf(M - p.x) + p.y;
-        M = p.x;
-      } else {
-        S += p.y * expf(p.x - M);
-      }
+      lse_fold(M, S, p.x, p.y);
     }
   }
-  red[wave][lane] = make_float2(M, S);
+  red[gi][e] = make_float2(M, S);
   __syncthreads();
-  if (wave == 0 && n < N) {
-    float Mt = -INFINITY;
+  if (gi == 0 && n < N) {
+    float Mt = -INFINITY, St = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) Mt = fmaxf(Mt, red[w][lane].x);
-    float St = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w)
-      if (red[w][lane].x != -INFINITY) St += red[w][lane].y * expf(red[w][lane].x - Mt);
+    for (int r = 0; r < CMB_G; ++r) lse_fold(Mt, St, red[r][e].x, red[r][e].y);
     const float lse = Mt + logf(St);
     // sequence of entry n: the last b with cu[b] <= n
     int lo = 0, hi = n_seqs - 1;
@@ -362,7 +469,8 @@ hipError_t launch_linear(int dtype, const void* x, const void* w, void* y, int M
     g.lda = K;
     g.ldb = K;
     g.tiles_n = (N + GBN - 1) / GBN;
-    const int tiles = ((M + GBM - 1) / GBM) * g.tiles_n;
+    g.tiles_m = (M + GBM - 1) / GBM;
+    const int tiles = g.tiles_m * g.tiles_n;
     EpiStore e{static_cast<u16*>(y), N};
     hipLaunchKernelGGL(gemm_tn_bf16<EpiStore>, dim3(tiles), dim3(GNT), 0, s, g, e);
     return hipGetLastError();
@@ -396,6 +504,7 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
     g.ldb = a.D;
     g.tiles_n = (a.N + GBN - 1) / GBN;
     n_vt = (a.V + GBM - 1) / GBM;
+    g.tiles_m = n_vt;
     EpiLse e{a.partial, a.target, a.ids};
     hipLaunchKernelGGL(gemm_tn_bf16<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
   } else {
@@ -414,7 +523,8 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(lse_combine, dim3((a.N + 63) / 64), dim3(256), 0, s, a.partial, n_vt,
+  hipLaunchKernelGGL(lse_combine, dim3((a.N + CMB_E - 1) / CMB_E), dim3(CMB_E * CMB_G), 0, s,
+                     a.partial, n_vt,
                      a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores, a.lse);
   return hipGetLastError();
 }
