@@ -15,7 +15,7 @@ LIB = os.path.join(HERE, "libcc.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["attention.hip", "gemm.hip", "select.hip", "compact.hip", "cc_api.hip"]
+SOURCES = ["attention.hip", "gemm.hip", "select.hip", "compact.hip", "fullpass.hip", "cc_api.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}",

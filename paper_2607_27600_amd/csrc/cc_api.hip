@@ -159,6 +159,35 @@ struct ScoreLayout {
   size_t attn, o, u, lm, total;
 };
 
+struct FullLayout {
+  size_t attn, rot, h, a, q, o, act, lm, total;
+};
+
+FullLayout full_layout(const cc_problem* p) {
+  FullLayout L;
+  const size_t N = n_tokens(p);
+  const size_t HD = size_t(p->n_heads_q) * p->head_dim;
+  size_t off = 0;
+  L.attn = off;
+  off += attention_ws_bytes(p);
+  L.rot = off;
+  off += align_up(N * (p->head_dim / 2) * sizeof(float2));
+  L.h = off;
+  off += align_up(N * p->hidden * sizeof(float));
+  L.a = off;
+  off += align_up(N * p->hidden * 2);
+  L.q = off;
+  off += align_up(N * HD * 2);
+  L.o = off;
+  off += align_up(N * HD * 2);
+  L.act = off;
+  off += align_up(N * size_t(p->ffn) * 2);
+  L.lm = off;
+  off += lmhead_ws_bytes(p);
+  L.total = off;
+  return L;
+}
+
 ScoreLayout score_layout(const cc_problem* p) {
   ScoreLayout L;
   const size_t N = n_tokens(p), es = esize(p->dtype);
@@ -177,11 +206,14 @@ ScoreLayout score_layout(const cc_problem* p) {
 
 char* at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
 
+// Attention over cache layer `layer`.  The work list is uploaded into `ws` unless an earlier
+// call of the same cc_score already did (upload = false).
 cc_status run_attention(const cc_problem* p, const void* q, const cc_kv* kv, int layer, void* o,
-                        void* ws, hipStream_t s) {
+                        void* ws, hipStream_t s, bool upload = true) {
   std::vector<int4> work = attention_work(p);
   if (work.empty()) return CC_OK;
-  CC_HIP(hipMemcpyAsync(ws, work.data(), work.size() * sizeof(int4), hipMemcpyHostToDevice, s));
+  if (upload)
+    CC_HIP(hipMemcpyAsync(ws, work.data(), work.size() * sizeof(int4), hipMemcpyHostToDevice, s));
   AttnLaunch a;
   a.dtype = p->dtype;
   a.q = q;
@@ -231,6 +263,54 @@ cc_status check_ws(void* ws, size_t have, size_t need) {
   if (need > 0 && !ws) return CC_ERR_ARG;
   if (need > 0 && (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0) return CC_ERR_ARG;
   return CC_OK;
+}
+
+// Full L-layer pass (Sec. 3.1): h = E[x]; per layer a = RMSNorm(h), q = RoPE(W_q a),
+// o = counter-causal attention on the stored K_l, V_l, h += W_o o, b = RMSNorm(h),
+// h += W_down (silu(W_gate b) * W_up b); then u = RMSNorm(h) and the LM head.
+cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, void* ws,
+                     size_t ws_bytes, void* stream) {
+  CC_TRY(check_kv(p, &in->kv, p->n_layers));
+  const int N = n_tokens(p);
+  if (N > 0 && (!in->embed || !in->layers_h || !in->final_norm || !in->w_lm || !in->token_ids ||
+                !scores))
+    return CC_ERR_ARG;
+  if (N > 0) {
+    if (!aligned16(in->embed) || !aligned16(in->w_lm) || !aligned16(in->final_norm))
+      return CC_ERR_ARG;
+    for (int l = 0; l < p->n_layers; ++l) {
+      const cc_layer_weights& W = in->layers_h[l];
+      const void* ptrs[7] = {W.attn_norm, W.wq, W.wo, W.mlp_norm, W.w_gate, W.w_up, W.w_down};
+      for (const void* q : ptrs)
+        if (!q || !aligned16(q)) return CC_ERR_ARG;
+    }
+  }
+  const FullLayout L = full_layout(p);
+  CC_TRY(check_ws(ws, ws_bytes, L.total));
+  if (N == 0) return CC_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int D = p->hidden, F = p->ffn, HD = p->n_heads_q * p->head_dim;
+  float2* rot = reinterpret_cast<float2*>(at(ws, L.rot));
+  float* h = reinterpret_cast<float*>(at(ws, L.h));
+  void* a = at(ws, L.a);
+  void* q = at(ws, L.q);
+  void* o = at(ws, L.o);
+  void* act = at(ws, L.act);
+  CC_HIP(launch_rope_table(in->pos_ids, p->cu_seqlens_d, p->n_seqs, rot, N, p->head_dim,
+                           double(p->rope_theta), s));
+  CC_HIP(launch_embed(in->embed, in->token_ids, h, N, D, s));
+  for (int l = 0; l < p->n_layers; ++l) {
+    const cc_layer_weights& W = in->layers_h[l];
+    CC_HIP(launch_rmsnorm(h, W.attn_norm, a, N, D, p->rms_eps, s));
+    CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, s));
+    CC_TRY(run_attention(p, q, &in->kv, l, o, at(ws, L.attn), s, l == 0));
+    CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, s));
+    CC_HIP(launch_rmsnorm(h, W.mlp_norm, a, N, D, p->rms_eps, s));
+    CC_HIP(launch_gate_up_swiglu(W.w_gate, W.w_up, a, act, N, D, F, s));
+    CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
+  }
+  CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
+  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
 }
 
 }  // namespace
@@ -303,8 +383,7 @@ cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_
 cc_status cc_score_workspace(const cc_problem* p, size_t* bytes) {
   if (!bytes) return CC_ERR_ARG;
   CC_TRY(check_problem(p));
-  if (p->mode == CC_MODE_FULL) return CC_ERR_UNSUPPORTED;
-  *bytes = score_layout(p).total;
+  *bytes = p->mode == CC_MODE_FULL ? full_layout(p).total : score_layout(p).total;
   return CC_OK;
 }
 
@@ -312,7 +391,7 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
                    size_t ws_bytes, void* stream) {
   CC_TRY(check_problem(p));
   if (!in) return CC_ERR_ARG;
-  if (p->mode == CC_MODE_FULL) return CC_ERR_UNSUPPORTED;
+  if (p->mode == CC_MODE_FULL) return score_full(p, in, scores, ws, ws_bytes, stream);
   CC_TRY(check_kv(p, &in->kv, 1));
   const int N = n_tokens(p);
   if (N > 0 && (!in->q || !in->w_o || !in->w_lm || !in->token_ids || !scores)) return CC_ERR_ARG;

@@ -142,6 +142,24 @@ struct CompactLaunch {
 };
 hipError_t launch_compact(const CompactLaunch& a, hipStream_t s);
 
-// FULL-mode building blocks.
-struct FullLaunch;  // defined in fullpass.hip
+// FULL-mode building blocks (bf16, head_dim 128).
+// q[n][:] = RoPE(W_q a[n]) with rot[n][e] = (cos, sin) of the entry's rotation angle.
+hipError_t launch_qproj_rope(const void* wq, const void* a, void* q, const float2* rot, int N,
+                             int D, int HD, hipStream_t s);
+// h[m][:] += x[m][:] W^T (fp32 residual stream).
+hipError_t launch_linear_residual(const void* x, const void* w, float* h, int M, int N, int K,
+                                  hipStream_t s);
+// act[n][f] = silu(W_gate b[n])[f] * (W_up b[n])[f].
+hipError_t launch_gate_up_swiglu(const void* w_gate, const void* w_up, const void* b, void* act,
+                                 int N, int D, int F, hipStream_t s);
+// h[n][:] = embed[ids[n]][:] (bf16 -> fp32).
+hipError_t launch_embed(const void* embed, const int32_t* ids, float* h, int N, int D,
+                        hipStream_t s);
+// y[n][:] = bf16(h[n][:] / sqrt(mean(h[n]^2) + eps) * gamma).
+hipError_t launch_rmsnorm(const float* h, const void* gamma, void* y, int N, int D, float eps,
+                          hipStream_t s);
+// rot[n][e] = (cos, sin)(pos[n] * theta^(-2e/head_dim)), e < head_dim/2, computed in fp64.
+// pos == null: positions 0..n_b-1 within each sequence.
+hipError_t launch_rope_table(const int32_t* pos, const int32_t* cu, int n_seqs, float2* rot,
+                             int N, int head_dim, double theta, hipStream_t s);
 }  // namespace cc

@@ -33,6 +33,7 @@ struct GemmArgs {
   int M, N, K;
   int64_t lda, ldb;
   int tiles_m, tiles_n;
+  const u16* A2;   // gated loader: logical A rows alternate in blocks of 32 between A and A2
 };
 
 __device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<const uint4*>(p); }
@@ -147,6 +148,111 @@ struct EpiLse {
   }
 };
 
+// M = query-projection rows (head-major, head_dim 128), N = entries.  Applies the
+// rotate-half rotary embedding at each entry's position (pairs (e, e+64) of a head are
+// blocks mb and mb+2 of the same lane: a wave's 128 rows are exactly one head) and
+// stores q[n][m] as bf16, token-major.
+struct EpiRope {
+  u16* out;            // [N][M]
+  const float2* rot;   // [N][64] (cos, sin) of position * theta^(-2e/128)
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    (void)tm;
+    (void)lds;
+    const int hi = lane >> 5, col = lane & 31;
+    if (m0w >= g.M) return;
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) {
+      const int n = n0w + nb * 32 + col;
+      if (n >= g.N) continue;
+      u16* orow = out + int64_t(n) * g.M + m0w;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          float lo[4], up[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int e = mb * 32 + jj * 8 + hi * 4 + i;   // 0..63
+            const float2 cs = rot[int64_t(n) * 64 + e];
+            const float a = acc[mb][nb][jj * 4 + i], b = acc[mb + 2][nb][jj * 4 + i];
+            lo[i] = a * cs.x - b * cs.y;
+            up[i] = b * cs.x + a * cs.y;
+          }
+          const int e0 = mb * 32 + jj * 8 + hi * 4;
+          uint2 v;
+          v.x = pack_bf2(lo[0], lo[1]);
+          v.y = pack_bf2(lo[2], lo[3]);
+          *reinterpret_cast<uint2*>(orow + e0) = v;
+          v.x = pack_bf2(up[0], up[1]);
+          v.y = pack_bf2(up[2], up[3]);
+          *reinterpret_cast<uint2*>(orow + e0 + 64) = v;
+        }
+    }
+  }
+};
+
+// M = entries, N = model width: the fp32 residual stream takes h[m][n] += acc.
+struct EpiResidual {
+  float* h;   // [M][N]
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    (void)tm;
+    (void)lds;
+    const int hi = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int n = n0w + nb * 32 + col;
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+          if (m < g.M) h[int64_t(m) * g.N + n] += acc[mb][nb][e];
+        }
+      }
+  }
+};
+
+// M = interleaved gate/up rows (see the gated loader), N = entries:
+// act[n][f] = silu(gate) * up, bf16, token-major [N][F].
+struct EpiSwiglu {
+  u16* act;
+  int F;
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    (void)tm;
+    (void)lds;
+    const int hi = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int pr = 0; pr < GMB / 2; ++pr) {
+      const int r0 = m0w + pr * 64;            // logical row of this gate block
+      if (r0 >= g.M) continue;
+      const int f0 = (r0 >> 6) * 32;
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int n = n0w + nb * 32 + col;
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          float o[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float gt = acc[2 * pr][nb][jj * 4 + i];
+            const float up = acc[2 * pr + 1][nb][jj * 4 + i];
+            o[i] = gt / (1.f + expf(-gt)) * up;
+          }
+          uint2 v;
+          v.x = pack_bf2(o[0], o[1]);
+          v.y = pack_bf2(o[2], o[3]);
+          *reinterpret_cast<uint2*>(act + int64_t(n) * F + f0 + jj * 8 + hi * 4) = v;
+        }
+      }
+    }
+  }
+};
+
 // Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8 XCDs (each
 // with its own L2), so consecutive logical tiles are first given to one XCD, then the
 // logical order walks groups of GROUP_M tile rows with the row index fastest: the ~32
@@ -174,7 +280,7 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 #define SCHED_DS_READ 0x100
 #define SCHED_DS_WRITE 0x200
 
-template <class Epi>
+template <class Epi, bool GATED = false>
 __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   __shared__ __attribute__((aligned(16))) u16 lds[2 * (GBM + GBN) * GLS];
   int tm, tn;
@@ -191,8 +297,17 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   const u16* pa[RA];
   const u16* pb[RB];
 #pragma unroll
-  for (int i = 0; i < RA; ++i)
-    pa[i] = g.A + int64_t(min(m0 + lr + RSTEP * i, g.M - 1)) * g.lda + lc * 8;
+  for (int i = 0; i < RA; ++i) {
+    const int r = min(m0 + lr + RSTEP * i, g.M - 1);
+    if constexpr (GATED) {
+      // rows [64j, 64j+32) are W_gate rows [32j, 32j+32), rows [64j+32, 64j+64) the same
+      // W_up rows, so each wave's 32-row MFMA blocks pair gate and up for one column range
+      const u16* base = ((r >> 5) & 1) ? g.A2 : g.A;
+      pa[i] = base + int64_t((r >> 6) * 32 + (r & 31)) * g.lda + lc * 8;
+    } else {
+      pa[i] = g.A + int64_t(r) * g.lda + lc * 8;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < RB; ++i)
     pb[i] = g.B + int64_t(min(n0 + lr + RSTEP * i, g.N - 1)) * g.ldb + lc * 8;
@@ -461,6 +576,7 @@ hipError_t launch_linear(int dtype, const void* x, const void* w, void* y, int M
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == CC_BF16) {
     GemmArgs g;
+    g.A2 = nullptr;
     g.A = static_cast<const u16*>(x);
     g.B = static_cast<const u16*>(w);
     g.M = M;
@@ -495,6 +611,7 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
   int n_vt;
   if (a.dtype == CC_BF16) {
     GemmArgs g;
+    g.A2 = nullptr;
     g.A = static_cast<const u16*>(a.w_lm);
     g.B = static_cast<const u16*>(a.u);
     g.M = a.V;
@@ -526,6 +643,53 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
   hipLaunchKernelGGL(lse_combine, dim3((a.N + CMB_E - 1) / CMB_E), dim3(CMB_E * CMB_G), 0, s,
                      a.partial, n_vt,
                      a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores, a.lse);
+  return hipGetLastError();
+}
+
+namespace {
+GemmArgs make_args(const void* a, const void* b, int M, int N, int K, int64_t lda, int64_t ldb) {
+  GemmArgs g;
+  g.A = static_cast<const u16*>(a);
+  g.B = static_cast<const u16*>(b);
+  g.A2 = nullptr;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.tiles_m = (M + GBM - 1) / GBM;
+  g.tiles_n = (N + GBN - 1) / GBN;
+  return g;
+}
+}  // namespace
+
+hipError_t launch_qproj_rope(const void* wq, const void* a, void* q, const float2* rot, int N,
+                             int D, int HD, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  GemmArgs g = make_args(wq, a, HD, N, D, D, D);
+  EpiRope e{static_cast<u16*>(q), rot};
+  hipLaunchKernelGGL(gemm_tn_bf16<EpiRope>, dim3(g.tiles_m * g.tiles_n), dim3(GNT), 0, s, g, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_linear_residual(const void* x, const void* w, float* h, int M, int N, int K,
+                                  hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  GemmArgs g = make_args(x, w, M, N, K, K, K);
+  EpiResidual e{h};
+  hipLaunchKernelGGL(gemm_tn_bf16<EpiResidual>, dim3(g.tiles_m * g.tiles_n), dim3(GNT), 0, s, g,
+                     e);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_up_swiglu(const void* w_gate, const void* w_up, const void* b, void* act,
+                                 int N, int D, int F, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  GemmArgs g = make_args(w_gate, b, 2 * F, N, D, D, D);
+  g.A2 = static_cast<const u16*>(w_up);
+  EpiSwiglu e{static_cast<u16*>(act), F};
+  hipLaunchKernelGGL((gemm_tn_bf16<EpiSwiglu, true>), dim3(g.tiles_m * g.tiles_n), dim3(GNT), 0,
+                     s, g, e);
   return hipGetLastError();
 }
 

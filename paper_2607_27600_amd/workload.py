@@ -59,6 +59,19 @@ class Workload:
         else:
             self.q = None
             self.w_o = None
+            emb = C.draw_embed(cfg)
+            self.embed = to_device(emb, device)
+            fn = C.final_norm(cfg)
+            self.final_norm = to_device(fn, device)
+            self.layers = []
+            host_layers = []
+            for l in range(cfg.n_layers):
+                W = C.draw_layer_weights(cfg, l)
+                self.layers.append({k: to_device(v, device) for k, v in W.items()})
+                if keep_host:
+                    host_layers.append(W)
+            if keep_host:
+                self.host.update(embed=emb, final_norm=fn, layers=host_layers)
         if with_lm_head:
             wlm = C.draw_wlm(cfg)
             self.w_lm = to_device(wlm, device)
@@ -114,11 +127,16 @@ class Workload:
                         dst[b, l, :, : hi - lo].copy_(to_device(np.ascontiguousarray(src[:, lo:hi]), "cpu"))
                     if keep_host and l == L - 1:
                         self.host[which] = src
+                    if keep_host and cfg.mode == "full":
+                        self.host.setdefault("kv_layers", {}).setdefault(l, {})[which] = src
             self.kv = cc.kv_contiguous(self.k_cache, self.v_cache, n_layers=L,
                                        seq_stride=L * hkv * cap * d, layer_stride=hkv * cap * d,
                                        head_stride=cap * d, tok_stride=d)
 
     def inputs(self) -> cc.Inputs:
+        if self.cfg.mode == "full":
+            return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=self.w_lm, embed=self.embed,
+                             layers=self.layers, final_norm=self.final_norm)
         return cc.inputs(q=self.q, kv=self.kv, token_ids=self.ids, w_o=self.w_o, w_lm=self.w_lm)
 
     def keep_budget(self) -> list:

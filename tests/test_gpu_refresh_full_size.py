@@ -1,0 +1,135 @@
+"""Whole refreshes at the full workload sizes, in the launch configuration the benchmark
+uses: scores on sampled rows against the oracle (rows are independent, so each sampled
+row is exact on its own), keep lists bit-exact against the oracle's selection on the
+GPU's own scores, and compaction checked byte for byte on sampled cache planes.
+
+  C3  n = 32768, Llama-3-8B shapes, keep 4096 per KV head, 32-layer cache in place
+  C5  8 ragged sequences (2048..16384), Qwen2.5-7B shapes, paged P=16 pool, keep 20%
+  C4  full 32-layer pass at n = 8192 (random 8B-shaped stack), keep 25%"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cc_oracle as O
+from synth import configs as C
+from tests.gpu_util import assert_scores_close, bf16_host
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _select_and_check(w, scores_d, per_head):
+    from paper_2607_27600_amd import cc
+    cfg = w.cfg
+    cu = cfg.cu_seqlens
+    hkv = cfg.n_heads_kv
+    starts, lens, ks = [], [], []
+    for b in range(cfg.n_seqs):
+        for _ in range(hkv if per_head else 1):
+            starts.append(int(cu[b]))
+            lens.append(int(cu[b + 1] - cu[b]))
+            ks.append(int(cfg.keep[b]))
+    keep = torch.empty(sum(ks), dtype=torch.int32, device="cuda")
+    cc.cc_select_keep(scores_d, starts, lens, ks, keep)
+    torch.cuda.synchronize()
+    got = keep.cpu().numpy()
+    s = scores_d.cpu().numpy()
+    off = 0
+    lists = []
+    for st, n, k in zip(starts, lens, ks):
+        ref = O.select_keep(s[st:st + n], k)
+        np.testing.assert_array_equal(got[off:off + k], ref)
+        lists.append(ref)
+        off += k
+    return keep, ks, lists
+
+
+def _check_planes(before_k, after_k, lists, cfg, per_head, paged, bt=None, n_check=6):
+    """Compare a few (sequence, layer, head) planes of the compacted keys with the gather."""
+    r = np.random.default_rng(0)
+    hkv = cfg.n_heads_kv
+    L = before_k.shape[0] if paged else before_k.shape[1]
+    for _ in range(n_check):
+        b = int(r.integers(0, cfg.n_seqs))
+        l = int(r.integers(0, L))
+        h = int(r.integers(0, hkv))
+        lst = lists[b * hkv + h] if per_head else lists[b]
+        if paged:
+            P = cfg.page_size
+            src = np.stack([before_k[l, bt[b, t // P], h, t % P] for t in lst])
+            dst = np.stack([after_k[l, bt[b, j // P], h, j % P] for j in range(len(lst))])
+        else:
+            src = O.compact(before_k[b, l, h], lst)
+            dst = after_k[b, l, h, :len(lst)]
+        np.testing.assert_array_equal(dst, src)
+
+
+def test_c3_long_context_refresh():
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.C3
+    print("[C3] building 32-layer cache, n=32768", flush=True)
+    w = Workload(cfg, keep_host=True)
+    scores = torch.empty(cfg.n_tokens, dtype=torch.float32, device="cuda")
+    cc.cc_score(w.problem, w.inputs(), scores)
+    torch.cuda.synchronize()
+    rows = C.sample_rows(cfg, count=48)
+    h = w.host
+    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                              cfg.cu_seqlens, rows=rows)
+    print("[C3] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C3"))
+    keep, ks, lists = _select_and_check(w, scores, per_head=True)
+    for hh in range(1, cfg.n_heads_kv):
+        np.testing.assert_array_equal(lists[hh], lists[0])
+    k_before = bf16_host(w.k_cache)
+    ids_before = w.ids.cpu().numpy()
+    cc.cc_compact_kv(w.problem, w.kv, keep, ks, 1, w.ids)
+    torch.cuda.synchronize()
+    _check_planes(k_before, bf16_host(w.k_cache), lists, cfg, True, False)
+    np.testing.assert_array_equal(w.ids.cpu().numpy()[:ks[0]], ids_before[lists[0]])
+
+
+def test_c5_ragged_paged_refresh():
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.C5
+    print(f"[C5] lens={cfg.seq_lens}", flush=True)
+    w = Workload(cfg, keep_host=True)
+    scores = torch.empty(cfg.n_tokens, dtype=torch.float32, device="cuda")
+    cc.cc_score(w.problem, w.inputs(), scores)
+    torch.cuda.synchronize()
+    rows = C.sample_rows(cfg, count=64)
+    h = w.host
+    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                              cfg.cu_seqlens, rows=rows)
+    print("[C5] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C5"))
+    keep, ks, lists = _select_and_check(w, scores, per_head=False)
+    k_before = bf16_host(w.k_cache)
+    cc.cc_compact_kv(w.problem, w.kv, keep, ks, 0, w.ids)
+    torch.cuda.synchronize()
+    _check_planes(k_before, bf16_host(w.k_cache), lists, cfg, False, True,
+                  bt=w.block_table.cpu().numpy())
+
+
+@pytest.mark.timeout(900)
+def test_c4_full_pass_refresh():
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.C4
+    print("[C4] drawing the 32-layer stack", flush=True)
+    w = Workload(cfg, keep_host=True)
+    scores = torch.empty(cfg.n_tokens, dtype=torch.float32, device="cuda")
+    cc.cc_score(w.problem, w.inputs(), scores)
+    torch.cuda.synchronize()
+    print("[C4] GPU pass done; oracle on sampled rows", flush=True)
+    rows = C.sample_rows(cfg, count=24)
+    h = w.host
+    kvl = h["kv_layers"]
+    ref = O.full_scores(h["ids"], lambda l: (kvl[l]["k"], kvl[l]["v"]), lambda l: h["layers"][l],
+                        h["embed"], h["final_norm"], h["w_lm"], cfg.cu_seqlens, cfg.n_layers,
+                        cfg.n_heads_q, cfg.head_dim, cfg.rope_theta, cfg.rms_eps, rows=rows)
+    print("[C4] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C4"))
+    keep, ks, lists = _select_and_check(w, scores, per_head=False)
+    k_before = bf16_host(w.k_cache)
+    cc.cc_compact_kv(w.problem, w.kv, keep, ks, 0, w.ids)
+    torch.cuda.synchronize()
+    _check_planes(k_before, bf16_host(w.k_cache), lists, cfg, False, False)
