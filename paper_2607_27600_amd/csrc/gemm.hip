@@ -25,7 +25,6 @@ constexpr int GBM = 256, GBN = 256, GBK = 64;
 constexpr int WGM = 2, WGN = 2, GNT = WGM * WGN * 64;
 constexpr int GTM = GBM / WGM, GTN = GBN / WGN;      // 128 x 128 per wave
 constexpr int GMB = GTM / 32, GNB = GTN / 32;        // 4 x 4 MFMA blocks
-constexpr int GLS = GBK + 8;                         // LDS row stride (elements)
 
 struct GemmArgs {
   const u16* A;
@@ -62,57 +61,54 @@ struct EpiStore {
 };
 
 // M = vocabulary, N = cached entries.  Writes partial[tm * N + n] = (max, sumexp) over
-// the workgroup's 256 vocabulary rows, and target[n] when ids[n] falls in them.
+// the workgroup's 256 vocabulary rows.  The whole epilogue runs while the matrix cores
+// idle, so it is kept to one max and one exp-accumulate per logit; only workgroups on the
+// vocabulary edge take the masked variant.
 struct EpiLse {
   float2* partial;
-  float* target;
-  const int32_t* ids;
+  template <bool EDGE>
+  __device__ __forceinline__ void reduce(const f32x16 (&acc)[GMB][GNB], int M, int m0w, int hi,
+                                         float (&mx)[GNB], float (&sm)[GNB]) const {
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) mx[nb] = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const bool ok = !EDGE || (m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3) < M);
+#pragma unroll
+        for (int nb = 0; nb < GNB; ++nb)
+          if (ok) mx[nb] = fmaxf(mx[nb], acc[mb][nb][e]);
+      }
+    float mc[GNB];
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) {
+      // a lane whose rows are all past the edge keeps max = -inf and sum = 0
+      mc[nb] = mx[nb] == -INFINITY ? 0.f : mx[nb] * kLog2e;
+      sm[nb] = 0.f;
+    }
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const bool ok = !EDGE || (m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3) < M);
+#pragma unroll
+        for (int nb = 0; nb < GNB; ++nb)
+          if (ok) sm[nb] += exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
+      }
+  }
+
   __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
                              int n0w, int lane, u16* lds) const {
     const int hi = lane >> 5, col = lane & 31;
     const int wave = threadIdx.x >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
-    __syncthreads();   // LDS tiles are no longer read
-    int id[GNB];
     float mx[GNB], sm[GNB];
-#pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) {
-      const int n = n0w + nb * 32 + col;
-      id[nb] = n < g.N ? ids[n] : -1;
-      mx[nb] = -INFINITY;
-      sm[nb] = 0.f;
-    }
-    // pass 1: per-entry max over this lane's vocabulary rows, and the target logit
-#pragma unroll
-    for (int mb = 0; mb < GMB; ++mb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-        const bool mv = m < g.M;
-#pragma unroll
-        for (int nb = 0; nb < GNB; ++nb) {
-          const float z = acc[mb][nb][e];
-          mx[nb] = mv ? fmaxf(mx[nb], z) : mx[nb];
-          if (m == id[nb]) target[n0w + nb * 32 + col] = z;
-        }
-      }
-    // pass 2: sum of exp(z - max)
-    float mc[GNB];
-#pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) mc[nb] = mx[nb] * kLog2e;
-#pragma unroll
-    for (int mb = 0; mb < GMB; ++mb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-        const bool mv = m < g.M;
-#pragma unroll
-        for (int nb = 0; nb < GNB; ++nb) {
-          const float t = exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
-          sm[nb] += mv ? t : 0.f;
-        }
-      }
+    if (tm * GBM + GBM <= g.M)
+      reduce<false>(acc, g.M, m0w, hi, mx, sm);
+    else
+      reduce<true>(acc, g.M, m0w, hi, mx, sm);
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
       // combine the two lane halves (rows 4*hi..)
@@ -253,22 +249,17 @@ struct EpiSwiglu {
   }
 };
 
-// Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8 XCDs (each
-// with its own L2), so consecutive logical tiles are first given to one XCD, then the
-// logical order walks groups of GROUP_M tile rows with the row index fastest: the ~32
-// workgroups an XCD runs at once cover a 4 x 8 block of tiles and share their A and B
-// k-slices in that XCD's L2.
+// Workgroup -> output tile: groups of GROUP_M tile rows, walked with the row index
+// fastest, so the workgroups in flight on the chip cover a few rows of tiles (sharing the
+// A tiles) times many columns (sharing each B tile) and find most k-slices in L2.
+// (Partitioning the order by XCD measured no better.)
 constexpr int GROUP_M = 4;
 
 __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int T = tiles_m * tiles_n;
-  const int per = T / 8, rem = T % 8;
-  const int x = bid % 8, j = bid / 8;
-  const int L = x * per + min(x, rem) + j;
-  const int group = L / (GROUP_M * tiles_n);
+  const int group = bid / (GROUP_M * tiles_n);
   const int first = group * GROUP_M;
   const int gsize = min(GROUP_M, tiles_m - first);
-  const int within = L - group * GROUP_M * tiles_n;
+  const int within = bid - group * GROUP_M * tiles_n;
   tm = first + within % gsize;
   tn = within / gsize;
 }
@@ -280,9 +271,23 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 #define SCHED_DS_READ 0x100
 #define SCHED_DS_WRITE 0x200
 
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_void;
+constexpr int STAGE = (GBM + GBN) * GBK;   // bf16 elements per LDS stage (64 KB)
+
+// The main loop.  Operand tiles go from global memory straight into LDS
+// (global_load_lds_dwordx4: lane i of a wave instruction fills bytes 16i..16i+15 of a 1 KB
+// run), so no registers stage them and no LDS write instructions are issued.  Tiles are
+// unpadded [rows][64] bf16 with the 16-byte chunk c of row r stored at chunk c ^ (r & 7):
+// the MFMA fragment reads of 8 consecutive rows then hit 8 distinct bank groups.  Two
+// stages are distinct LDS objects so the compiler can tell the stage being filled from the
+// stage being read (a shared object would make it wait for the loads before every read).
+// One barrier per k-tile, placed after the step-3 fragments are read: past it, the next
+// stage is complete and the current one is free for the loads of the tile after next.
 template <class Epi, bool GATED = false>
 __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
-  __shared__ __attribute__((aligned(16))) u16 lds[2 * (GBM + GBN) * GLS];
+  __shared__ __attribute__((aligned(1024))) u16 lds0[STAGE];
+  __shared__ __attribute__((aligned(1024))) u16 lds1[STAGE];
   int tm, tn;
   tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
   const int m0 = tm * GBM, n0 = tn * GBN;
@@ -290,56 +295,51 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   const int hi = lane >> 5, col = lane & 31;
   const int wm = wave / WGN, wn = wave % WGN;
 
-  constexpr int RA = GBM * 8 / GNT, RB = GBN * 8 / GNT, RSTEP = GNT / 8;
-  const int lc = tid & 7, lr = tid >> 3;
-  // Rows past the matrix edge are clamped to the last row: their products land in output
-  // rows/columns the epilogues discard, so no zero fill (and no branch) is needed.
-  const u16* pa[RA];
-  const u16* pb[RB];
+  // wave w, load instruction j covers tile rows (8w + j) * 8 .. +8; rows past the matrix
+  // edge are clamped to the last row (their products land in outputs the epilogues
+  // discard), so the loop has no branches
+  const u16* ga[8];
+  const u16* gb[8];
 #pragma unroll
-  for (int i = 0; i < RA; ++i) {
-    const int r = min(m0 + lr + RSTEP * i, g.M - 1);
+  for (int j = 0; j < 8; ++j) {
+    const int r = (wave * 8 + j) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7);
+    const int ra = min(m0 + r, g.M - 1);
     if constexpr (GATED) {
-      // rows [64j, 64j+32) are W_gate rows [32j, 32j+32), rows [64j+32, 64j+64) the same
+      // rows [64i, 64i+32) are W_gate rows [32i, 32i+32), rows [64i+32, 64i+64) the same
       // W_up rows, so each wave's 32-row MFMA blocks pair gate and up for one column range
-      const u16* base = ((r >> 5) & 1) ? g.A2 : g.A;
-      pa[i] = base + int64_t((r >> 6) * 32 + (r & 31)) * g.lda + lc * 8;
+      const u16* base = ((ra >> 5) & 1) ? g.A2 : g.A;
+      ga[j] = base + int64_t((ra >> 6) * 32 + (ra & 31)) * g.lda + c * 8;
     } else {
-      pa[i] = g.A + int64_t(r) * g.lda + lc * 8;
+      ga[j] = g.A + int64_t(ra) * g.lda + c * 8;
     }
+    gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8;
   }
+  auto issue = [&](u16* stage, int k0) {
+    u16* base = stage + wave * 8 * 512;
 #pragma unroll
-  for (int i = 0; i < RB; ++i)
-    pb[i] = g.B + int64_t(min(n0 + lr + RSTEP * i, g.N - 1)) * g.ldb + lc * 8;
-  uint4 ra[RA], rbv[RB];
-
-  auto gload = [&](int k0) {
+    for (int j = 0; j < 8; ++j)
+      __builtin_amdgcn_global_load_lds((global_void*)(ga[j] + k0), (lds_void*)(base + j * 512),
+                                       16, 0, 0);
 #pragma unroll
-    for (int i = 0; i < RA; ++i) ra[i] = ld16(pa[i] + k0);
-#pragma unroll
-    for (int i = 0; i < RB; ++i) rbv[i] = ld16(pb[i] + k0);
+    for (int j = 0; j < 8; ++j)
+      __builtin_amdgcn_global_load_lds((global_void*)(gb[j] + k0),
+                                       (lds_void*)(base + GBM * GBK + j * 512), 16, 0, 0);
   };
-  auto lstore = [&](int buf) {
-    u16* As = lds + buf * (GBM + GBN) * GLS;
-    u16* Bs = As + GBM * GLS;
+  auto fread = [&](const u16* As, int ks, bf16x8 (&fa)[GMB], bf16x8 (&fb)[GNB]) {
+    const u16* Bs = As + GBM * GBK;
+    const int c = 2 * ks + hi;
 #pragma unroll
-    for (int i = 0; i < RA; ++i)
-      *reinterpret_cast<uint4*>(As + (lr + RSTEP * i) * GLS + lc * 8) = ra[i];
+    for (int mb = 0; mb < GMB; ++mb) {
+      const int r = wm * GTM + mb * 32 + col;
+      fa[mb] = as_bf16x8(ld16(As + r * GBK + ((c ^ (r & 7)) * 8)));
+    }
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
-      *reinterpret_cast<uint4*>(Bs + (lr + RSTEP * i) * GLS + lc * 8) = rbv[i];
+    for (int nb = 0; nb < GNB; ++nb) {
+      const int r = wn * GTN + nb * 32 + col;
+      fb[nb] = as_bf16x8(ld16(Bs + r * GBK + ((c ^ (r & 7)) * 8)));
+    }
   };
-  auto fread = [&](int buf, int ks, bf16x8 (&fa)[GMB], bf16x8 (&fb)[GNB]) {
-    const u16* As = lds + buf * (GBM + GBN) * GLS;
-    const u16* Bs = As + GBM * GLS;
-#pragma unroll
-    for (int mb = 0; mb < GMB; ++mb)
-      fa[mb] = as_bf16x8(ld16(As + (wm * GTM + mb * 32 + col) * GLS + ks * 16 + hi * 8));
-#pragma unroll
-    for (int nb = 0; nb < GNB; ++nb)
-      fb[nb] = as_bf16x8(ld16(Bs + (wn * GTN + nb * 32 + col) * GLS + ks * 16 + hi * 8));
-  };
-
   f32x16 acc[GMB][GNB];
 #pragma unroll
   for (int mb = 0; mb < GMB; ++mb)
@@ -351,72 +351,51 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
 #pragma unroll
       for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = mfma32(fa[mb], fb[nb], acc[mb][nb]);
   };
-
+  // scheduling hint: one fragment read between consecutive MFMAs, then the rest
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
   const int nk = g.K / GBK;
   bf16x8 fa0[GMB], fb0[GNB], fa1[GMB], fb1[GNB];
-  gload(0);
-  lstore(0);
+  // one k-tile from `cur`; fragments of each step are read during the previous step
+  auto tile = [&](const u16* cur, u16* nxt, int kt) {
+    __builtin_amdgcn_sched_barrier(0);
+    fread(cur, 1, fa1, fb1);
+    mfmas(fa0, fb0);
+    interleave();
+    fread(cur, 2, fa0, fb0);
+    mfmas(fa1, fb1);
+    interleave();
+    fread(cur, 3, fa1, fb1);
+    mfmas(fa0, fb0);
+    interleave();
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads into `nxt` have landed
+    __syncthreads();                 // everyone's have, and everyone is done with `cur`
+    issue(const_cast<u16*>(cur), min(kt + 2, nk - 1) * GBK);   // past the end: a reload
+    fread(nxt, 0, fa0, fb0);
+    mfmas(fa1, fb1);
+    interleave();
+  };
+  issue(lds0, 0);
+  issue(lds1, min(1, nk - 1) * GBK);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  fread(0, 0, fa0, fb0);
-  if (nk > 1) gload(GBK);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    // k-step 0: read step-1 fragments while the step-0 MFMAs run
-    __builtin_amdgcn_sched_barrier(0);
-    fread(buf, 1, fa1, fb1);
-    mfmas(fa0, fb0);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    // k-step 1
-    fread(buf, 2, fa0, fb0);
-    mfmas(fa1, fb1);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    // k-step 2, then the next tile goes from registers to the other LDS buffer
-    fread(buf, 3, fa1, fb1);
-    mfmas(fa0, fb0);
-    lstore(buf ^ 1);   // on the last tile this fills a buffer nobody reads
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_DS_WRITE, 2, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
-    // k-step 3: fragments of the next tile's step 0 and the global loads two tiles ahead
-    // are issued between the MFMAs
-    fread(buf ^ 1, 0, fa0, fb0);
-    gload(min(kt + 2, nk - 1) * GBK);   // past the end: a harmless reload of the last tile
-    mfmas(fa1, fb1);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(SCHED_VMEM_READ, 2, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+  fread(lds0, 0, fa0, fb0);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    tile(lds0, lds1, kt);
+    tile(lds1, lds0, kt + 1);
   }
+  if (kt < nk) tile(lds0, lds1, kt);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds);
+  epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds0);
 }
 
 // ------------------------------------------------------------------ fp32 path
@@ -517,6 +496,32 @@ __global__ __launch_bounds__(256) void gemm_tn_f32(GemmArgsF g, Epi epi) {
 }
 
 // ------------------------------------------------------------------ LSE combine
+
+// The logit of the cached token, z_i[x_i] = W_lm[x_i] . u_i, one wave per entry with fp32
+// accumulation (the same products the LM-head GEMM accumulates, in another order).
+template <typename T>
+__device__ __forceinline__ float ldf(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float ldf<u16>(const u16* p, int64_t i) { return bf2f(p[i]); }
+template <>
+__device__ __forceinline__ float ldf<float>(const float* p, int64_t i) { return p[i]; }
+
+template <typename T>
+__global__ __launch_bounds__(256) void target_logit(const T* __restrict__ u,
+                                                    const T* __restrict__ w,
+                                                    const int32_t* __restrict__ ids,
+                                                    float* __restrict__ target, int N, int D) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const T* ur = u + int64_t(n) * D;
+  const T* wr = w + int64_t(ids[n]) * D;
+  float acc = 0.f;
+  for (int i = lane; i < D; i += 64) acc = fmaf(ldf<T>(ur, i), ldf<T>(wr, i), acc);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) target[n] = acc;
+}
 
 // One workgroup per 16 entries: thread (group gi, entry e) folds the vocabulary tiles
 // gi, gi+16, ... of entry e (16 consecutive entries read 128 contiguous bytes of a tile's
@@ -622,8 +627,12 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
     g.tiles_n = (a.N + GBN - 1) / GBN;
     n_vt = (a.V + GBM - 1) / GBM;
     g.tiles_m = n_vt;
-    EpiLse e{a.partial, a.target, a.ids};
+    EpiLse e{a.partial};
     hipLaunchKernelGGL(gemm_tn_bf16<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    hipLaunchKernelGGL(target_logit<u16>, dim3((a.N + 3) / 4), dim3(256), 0, s,
+                       static_cast<const u16*>(a.u), static_cast<const u16*>(a.w_lm), a.ids,
+                       a.target, a.N, a.D);
   } else {
     GemmArgsF g;
     g.A = static_cast<const float*>(a.w_lm);
