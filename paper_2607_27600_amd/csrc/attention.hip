@@ -16,10 +16,17 @@
 //   to match the MFMA k-slots of the P operand; both are double buffered with one
 //   barrier per tile.
 // fp32 path: one thread per row, K/V tiles staged in LDS, exact fp32 online softmax.
+#include <type_traits>
+
 #include "cc_internal.h"
 
 namespace cc {
 namespace {
+
+#define SCHED_VALU 0x002
+#define SCHED_MFMA 0x008
+#define SCHED_DS_READ 0x100
+#define SCHED_TRANS 0x400
 
 constexpr int BN = 64;            // keys per tile
 constexpr int HD = 128;           // head dim of the MFMA path
@@ -30,6 +37,7 @@ constexpr int KS = HD + 8;        // LDS row stride of K (elements): 272 B
 constexpr int VS = BN + 8;        // LDS row stride of V^T (elements): 144 B
 constexpr int K_TILE = BN * KS;
 constexpr int V_TILE = HD * VS;
+constexpr float kRescale = 8.f;   // log2 headroom before the softmax reference max moves
 
 struct AttnArgs {
   const u16* q;
@@ -47,7 +55,11 @@ __device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<c
 
 template <bool PAGED>
 __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) u16 lds[2 * (K_TILE + V_TILE)];
+  // K tiles run one tile ahead of V tiles: while the softmax of tile t runs on the VALU, the
+  // MFMAs of S for tile t+1 are already issued, so each wave overlaps its own softmax with
+  // matrix work.  Two K buffers (tiles t+1, t+2) and two V buffers (tiles t, t+1).
+  __shared__ __attribute__((aligned(16))) u16 kl[2][K_TILE];
+  __shared__ __attribute__((aligned(16))) u16 vl[2][V_TILE];
 
   const int4 w = a.work[blockIdx.x];
   const int b = w.x, kvh = w.y, rb = w.z;
@@ -78,53 +90,102 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
 
   const int row0 = rb * ROWS;
   const int pos_lo = row0 / g;
-  const int wlast = row0 + wave * ROWS_W + ROWS_W - 1;
-  const int pos_hi_w = wlast < nrows ? wlast / g : n;   // invalid rows need masking always
+  const int wg_last = min(row0 + ROWS, nrows) - 1;
+  const int pos_hi_wg = row0 + ROWS > nrows ? n : wg_last / g;   // partial blocks mask always
   const int first_key = pos_lo + (a.inclusive ? 0 : 1);
-  const int t_begin = first_key / BN;
-  const int t_end = (n + BN - 1) / BN;
+  const int tb = first_key / BN;
+  const int te = (n + BN - 1) / BN;
+  if (tb >= te) {
+    // no key reachable from any row of the block: every output row is 0
+    if (valid) {
+      u16* op = a.o + (int64_t(seq0 + pos) * a.hq + hq) * HD + hi * 4;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          *reinterpret_cast<uint2*>(op + db * 32 + jj * 8) = make_uint2(0, 0);
+    }
+    return;
+  }
+  // tiles [tb, tm0) and [tm1, te) need the mask; [tm0, tm1) see every key of every row
+  const int tm0 = min(te, max(tb, (pos_hi_wg + 1 + BN - 1) / BN));
+  const int tm1 = (n % BN == 0) ? te : te - 1;
 
   const u16* kbase = reinterpret_cast<const u16*>(a.k.base);
   const u16* vbase = reinterpret_cast<const u16*>(a.v.base);
 
-  // global -> register staging of one K/V tile
+  // global -> register staging
   // K: thread owns 16-byte column chunk kc of rows kr0 + 16*i.
   const int kc = tid & 15, kr0 = tid >> 4;
   // V: thread owns keys 4*vg .. 4*vg+3, dims 8*vd .. 8*vd+7.
   const int vg = tid & 15, vd = tid >> 4;
   uint4 kreg[4], vreg[4];
 
-  auto load_tile = [&](int t) {
-    const int key0 = t * BN;
+  // Row addressing.  Contiguous caches: this thread's rows of tile 0 are fixed pointers
+  // and a tile is a uniform (scalar) offset, so full tiles cost one add per row; only the
+  // last, partial tile clamps rows to n-1.  Paged caches: one block-table lookup per row.
+  const u16* kp[4];
+  const u16* vp[4];
+  if constexpr (!PAGED) {
+    const u16* kplane = kbase + kv_off<false>(a.k, b, a.layer, kvh, 0);
+    const u16* vplane = vbase + kv_off<false>(a.v, b, a.layer, kvh, 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = key0 + kr0 + 16 * i;
-      if (key < n) {
-        kreg[i] = ld16(kbase + kv_off<PAGED>(a.k, b, a.layer, kvh, key) + kc * 8);
-      } else {
-        kreg[i] = make_uint4(0, 0, 0, 0);
-      }
+      kp[i] = kplane + int64_t(kr0 + 16 * i) * a.k.tok_stride + kc * 8;
+      vp[i] = vplane + int64_t(4 * vg + i) * a.v.tok_stride + vd * 8;
     }
+  }
+  auto load_k = [&](int t) {
+    const int key0 = t * BN;   // rows past n are clamped to n-1 and masked
+    if constexpr (PAGED) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = key0 + 4 * vg + i;
-      if (key < n) {
-        vreg[i] = ld16(vbase + kv_off<PAGED>(a.v, b, a.layer, kvh, key) + vd * 8);
+      for (int i = 0; i < 4; ++i)
+        kreg[i] = ld16(kbase + kv_off<true>(a.k, b, a.layer, kvh, min(key0 + kr0 + 16 * i, n - 1)) +
+                       kc * 8);
+    } else {
+      if (key0 + BN <= n) {
+        const int64_t off = int64_t(key0) * a.k.tok_stride;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) kreg[i] = ld16(kp[i] + off);
       } else {
-        vreg[i] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = min(key0 + kr0 + 16 * i, n - 1);
+          kreg[i] = ld16(kp[i] + (int64_t(key - kr0 - 16 * i) * a.k.tok_stride));
+        }
       }
     }
   };
-
+  auto load_v = [&](int t) {
+    const int key0 = t * BN;
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = key0 + 4 * vg + i;
+        // value rows past n get zero (their weights are 0, but garbage could be NaN)
+        vreg[i] = key < n ? ld16(vbase + kv_off<true>(a.v, b, a.layer, kvh, key) + vd * 8)
+                          : make_uint4(0, 0, 0, 0);
+      }
+    } else {
+      const int64_t off = int64_t(key0) * a.v.tok_stride;
+      if (key0 + BN <= n) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) vreg[i] = ld16(vp[i] + off);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          vreg[i] = key0 + 4 * vg + i < n ? ld16(vp[i] + off) : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
   // position of key 4*vg within the permuted V^T row (see the PV operand layout below)
   const int vpos = (vg >> 2) * 16 + (vg & 1) * 8 + ((vg >> 1) & 1) * 4;
-
-  auto store_tile = [&](int buf) {
-    u16* Kl = lds + buf * (K_TILE + V_TILE);
-    u16* Vl = Kl + K_TILE;
+  auto store_k = [&](u16* Kl) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       *reinterpret_cast<uint4*>(Kl + (kr0 + 16 * i) * KS + kc * 8) = kreg[i];
+  };
+  auto store_v = [&](u16* Vl) {
     const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
     const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
     const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
@@ -143,96 +204,127 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     }
   };
 
+  // S^T[key][row] for the 64 keys of a tile: two 32-key blocks; 16 MFMAs, MFMA j uses
+  // key block j%2 and dims 16*(j/2) ..
+  auto kfrag = [&](const u16* Kl, int j) {
+    return as_bf16x8(ld16(Kl + ((j & 1) * 32 + col) * KS + (j >> 1) * 16 + hi * 8));
+  };
+  auto vfrag = [&](const u16* Vl, int j) {   // PV MFMA j: k-step j/4, d block j%4
+    return as_bf16x8(ld16(Vl + ((j & 3) * 32 + col) * VS + (j >> 2) * 16 + hi * 8));
+  };
+
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 acc[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) acc[db] = f32x16{};
 
-  if (t_begin < t_end) {
-    load_tile(t_begin);
-    store_tile(0);
-  }
+  // prologue: K(tb), V(tb) and K(tb+1) in LDS, S(tb) in registers
+  load_k(tb);
+  load_v(tb);
+  store_k(kl[0]);
+  store_v(vl[0]);
+  load_k(min(tb + 1, te - 1));
+  store_k(kl[1]);
   __syncthreads();
-
-  for (int t = t_begin; t < t_end; ++t) {
-    const int buf = (t - t_begin) & 1;
-    const bool more = t + 1 < t_end;
-    if (more) load_tile(t + 1);
-
-    const u16* Kl = lds + buf * (K_TILE + V_TILE);
-    const u16* Vl = Kl + K_TILE;
-
-    // S^T[key][row] for the 64 keys of the tile: two 32-key blocks.
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+  f32x16 s_cur[2], s_nxt[2];
+  s_cur[0] = f32x16{};
+  s_cur[1] = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        const bf16x8 kf = as_bf16x8(ld16(Kl + (mb * 32 + col) * KS + ks * 16 + hi * 8));
-        s[mb] = mfma32(kf, qf[ks], s[mb]);
-      }
-    }
+  for (int j = 0; j < 16; ++j) s_cur[j & 1] = mfma32(kfrag(kl[0], j), qf[j >> 1], s_cur[j & 1]);
 
-    const int key0 = t * BN;
-    if (key0 <= pos_hi_w || key0 + BN > n) {
+  // One tile.  S(t) is in s_cur; K(t+1) sits in kl[(t+1-tb)&1] and V(t) in vl[(t-tb)&1]; the
+  // loads of K(t+2), V(t+1) refill the buffers freed by K(t), V(t-1).  The step is written
+  // in the order it should issue (sched_barrier fences keep the compiler from regrouping):
+  // the 16 MFMAs of S(t+1) are spread over the exponentials of this tile's softmax, and the
+  // 16 MFMAs of P V over the LDS stores of the next tiles.  Past the last tile, loads and
+  // S are clamped to the last tile and land in buffers nobody reads.
+  auto step = [&](int t, auto mask_tag) {
+    constexpr bool kMask = decltype(mask_tag)::value;
+    const int i = t - tb;
+    const u16* Kn = kl[(i + 1) & 1];
+    const u16* Vc = vl[i & 1];
+    load_k(min(t + 2, te - 1));
+    load_v(min(t + 1, te - 1));
+    bf16x8 kf[4];
+    kf[0] = kfrag(Kn, 0);
+    kf[1] = kfrag(Kn, 1);
+    kf[2] = kfrag(Kn, 2);
+    if (kMask) {
+      const int key0 = t * BN;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = key0 + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
           const bool ok = key < n && (a.inclusive ? key >= pos : key > pos);
-          if (!ok) s[mb][e] = -INFINITY;
+          s_cur[mb][e] = ok ? s_cur[mb][e] : -INFINITY;
         }
     }
-
     float mx = -INFINITY;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[mb][e]);
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s_cur[mb][e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float mc = m_use * a.c2;
-    const float corr = exp2f(m_run * a.c2 - mc);
+    // Lazy rescaling: the reference max only moves when the row max grows by more than
+    // 2^8 in probability units (or on the first non-empty tile).  Numerator and
+    // denominator always share the reference, so the result is unchanged; p stays <= 256.
+    const bool up = mx > m_run + kRescale / a.c2;
+    const float corr = up ? fast_exp2((m_run - mx) * a.c2) : 1.f;   // 0 when m_run = -inf
+    m_run = up ? mx : m_run;
+    const float mc = (m_run == -INFINITY ? 0.f : m_run) * a.c2;
+    s_nxt[0] = f32x16{};
+    s_nxt[1] = f32x16{};
     float lsum = 0.f;
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int j = 0; j < 16; ++j) {
+      if (j + 3 < 16) kf[(j + 3) & 3] = kfrag(Kn, j + 3);
+      s_nxt[j & 1] = mfma32(kf[j & 3], qf[j >> 1], s_nxt[j & 1]);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = exp2f(fmaf(s[mb][e], a.c2, -mc));
-        s[mb][e] = p;
+      for (int u = 0; u < 2; ++u) {
+        const int f = 2 * j + u, mb = f >> 4, e = f & 15;
+        const float p = fast_exp2(fmaf(s_cur[mb][e], a.c2, -mc));
+        // pin the exponential here, between the MFMAs, instead of next to its later uses
+        asm volatile("" ::"v"(p));
+        s_cur[mb][e] = p;
         lsum += p;
       }
-    l_run = l_run * corr + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < 4; ++db) acc[db] *= corr;
-
-    // P^T operand: k-step kk covers keys 16*kk .. 16*kk+15; lane half hi holds keys
-    // {4hi..4hi+3, 8+4hi..8+4hi+3} of that step, i.e. S^T entries 8*(kk%2) .. +7 of block kk/2.
-    bf16x8 pf[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      uint4 pk;
-      const int mb = kk >> 1, e0 = (kk & 1) * 8;
-      pk.x = pack_bf2(s[mb][e0 + 0], s[mb][e0 + 1]);
-      pk.y = pack_bf2(s[mb][e0 + 2], s[mb][e0 + 3]);
-      pk.z = pack_bf2(s[mb][e0 + 4], s[mb][e0 + 5]);
-      pk.w = pack_bf2(s[mb][e0 + 6], s[mb][e0 + 7]);
-      pf[kk] = as_bf16x8(pk);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    l_run = l_run * corr + lsum;
+    // P^T operand: k-step kk covers keys 16*kk .. 16*kk+15; lane half hi holds keys
+    // {4hi..4hi+3, 8+4hi..8+4hi+3} of that step, i.e. S^T entries 8*(kk%2)..+7 of block kk/2
+    bf16x8 pf[4];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const bf16x8 vf = as_bf16x8(ld16(Vl + (db * 32 + col) * VS + kk * 16 + hi * 8));
-        acc[db] = mfma32(vf, pf[kk], acc[db]);
-      }
-
-    if (more) store_tile(buf ^ 1);
+      for (int e = 0; e < 8; ++e) pf[kk][e] = (__bf16)s_cur[kk >> 1][(kk & 1) * 8 + e];
+    if (__any(corr != 1.f)) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db) acc[db] *= corr;
+    }
+    bf16x8 vf[4];
+    vf[0] = vfrag(Vc, 0);
+    vf[1] = vfrag(Vc, 1);
+    vf[2] = vfrag(Vc, 2);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (j + 3 < 16) vf[(j + 3) & 3] = vfrag(Vc, j + 3);
+      acc[j & 3] = mfma32(vf[j & 3], pf[j >> 2], acc[j & 3]);
+      if (j == 7) store_k(kl[i & 1]);
+      if (j == 11) store_v(vl[(i + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     __syncthreads();
-  }
+    s_cur[0] = s_nxt[0];
+    s_cur[1] = s_nxt[1];
+  };
+  int t = tb;
+  for (; t < tm0; ++t) step(t, std::true_type{});
+  for (; t < tm1; ++t) step(t, std::false_type{});
+  for (; t < te; ++t) step(t, std::true_type{});
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -242,10 +334,10 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        uint2 o;
-        o.x = pack_bf2(acc[db][jj * 4 + 0] * inv, acc[db][jj * 4 + 1] * inv);
-        o.y = pack_bf2(acc[db][jj * 4 + 2] * inv, acc[db][jj * 4 + 3] * inv);
-        *reinterpret_cast<uint2*>(op + db * 32 + jj * 8) = o;
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (__bf16)(acc[db][jj * 4 + e] * inv);
+        *reinterpret_cast<bf16x4*>(op + db * 32 + jj * 8) = o;
       }
   }
 }

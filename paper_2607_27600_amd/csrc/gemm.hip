@@ -94,7 +94,7 @@ struct EpiLse {
         const bool ok = !EDGE || (m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3) < M);
 #pragma unroll
         for (int nb = 0; nb < GNB; ++nb)
-          if (ok) sm[nb] += exp2f(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
+          if (ok) sm[nb] += fast_exp2(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
       }
   }
 
