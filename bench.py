@@ -166,6 +166,18 @@ def main():
             part_ms[n] += e[j].elapsed_time(e[j + 1]) / args.steps
     ms_step = elapsed * 1e3 / args.steps
 
+    # in-place compaction (what a refresh does to the live cache), timed on its own after
+    # the steps: every call moves the same bytes
+    ev_ip = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    cc.cc_compact_kv(p, w.kv, keep, ks, int(cfg.per_head_select), workspace=ws_cmp)
+    torch.cuda.synchronize()
+    ev_ip[0].record(stream)
+    for _ in range(args.steps):
+        cc.cc_compact_kv(p, w.kv, keep, ks, int(cfg.per_head_select), workspace=ws_cmp)
+    ev_ip[1].record(stream)
+    torch.cuda.synchronize()
+    ip_ms = ev_ip[0].elapsed_time(ev_ip[1]) / args.steps
+
     att_flop = 2.0 * d * Hq * sum(n * (n - 1) for n in cfg.seq_lens)
     lm_flop = 2.0 * N * D * V
     wo_flop = 2.0 * N * D * Hq * d
@@ -199,6 +211,8 @@ def main():
                       "flop_per_launch": att_flop},
         "compact": {"gb_s": compact_gbs, "frac_hbm": compact_gbs / PEAK_HBM_GBS,
                     "bytes_moved": 2 * kept_bytes, "mode": "out of place, 32-layer cache"},
+        "compact_in_place": {"ms": ip_ms, "gb_s": 2 * kept_bytes / (ip_ms * 1e-3) / 1e9,
+                             "frac_hbm": 2 * kept_bytes / (ip_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "breakdown_ms": part_ms,
         "wo_proj_tflops": wo_flop / (part_ms["wo_proj"] * 1e-3) / 1e12,
         "input_generation_s": t_gen,

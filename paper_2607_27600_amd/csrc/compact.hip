@@ -50,15 +50,14 @@ __global__ __launch_bounds__(CNT) void compact_kernel(CompactArgs a) {
   int j_begin = IN_PLACE ? 0 : blockIdx.y * a.rows_per_chunk;
   int j_end = IN_PLACE ? k : min(k, j_begin + a.rows_per_chunk);
   for (int j0 = j_begin; j0 < j_end; j0 += a.rows_per_chunk) {
+    // branch-free gather: rows past the list end re-read its last entry and are not stored
+    int src[CU];
+#pragma unroll
+    for (int u = 0; u < CU; ++u) src[u] = keep[min(j0 + r0 + u * rstep, j_end - 1)];
     uint4 buf[CU];
 #pragma unroll
-    for (int u = 0; u < CU; ++u) {
-      const int j = j0 + r0 + u * rstep;
-      if (j < j_end) {
-        const int src = keep[j];
-        buf[u] = ldg16(sb + kv_off<PAGED>(sv, P.seq, P.layer, P.head, src) + esz16);
-      }
-    }
+    for (int u = 0; u < CU; ++u)
+      buf[u] = ldg16(sb + kv_off<PAGED>(sv, P.seq, P.layer, P.head, src[u]) + esz16);
     if (IN_PLACE) {
       __builtin_amdgcn_s_waitcnt(0);   // this thread's loads have returned
       __syncthreads();                 // ... and so have everyone's

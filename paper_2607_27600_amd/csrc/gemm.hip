@@ -517,7 +517,22 @@ __global__ __launch_bounds__(256) void target_logit(const T* __restrict__ u,
   const T* ur = u + int64_t(n) * D;
   const T* wr = w + int64_t(ids[n]) * D;
   float acc = 0.f;
-  for (int i = lane; i < D; i += 64) acc = fmaf(ldf<T>(ur, i), ldf<T>(wr, i), acc);
+  if constexpr (sizeof(T) == 2) {
+    // 16-byte loads: 8 bf16 per lane per step, all steps' loads independent
+    for (int i = lane * 8; i < D; i += 512) {
+      const uint4 a = *reinterpret_cast<const uint4*>(ur + i);
+      const uint4 b = *reinterpret_cast<const uint4*>(wr + i);
+      const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc = fmaf(__uint_as_float(av[q] << 16), __uint_as_float(bv[q] << 16), acc);
+        acc = fmaf(__uint_as_float(av[q] & 0xffff0000u), __uint_as_float(bv[q] & 0xffff0000u),
+                   acc);
+      }
+    }
+  } else {
+    for (int i = lane; i < D; i += 64) acc = fmaf(ldf<T>(ur, i), ldf<T>(wr, i), acc);
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (lane == 0) target[n] = acc;
@@ -547,7 +562,16 @@ __global__ __launch_bounds__(CMB_E * CMB_G) void lse_combine(const float2* parti
   const int n = blockIdx.x * CMB_E + e;
   float M = -INFINITY, S = 0.f;
   if (n < N) {
-    for (int t = gi; t < n_tiles; t += CMB_G) {
+    // eight independent loads in flight per thread, then fold
+    int t = gi;
+    for (; t + 7 * CMB_G < n_tiles; t += 8 * CMB_G) {
+      float2 p[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) p[q] = partial[int64_t(t + q * CMB_G) * N + n];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) lse_fold(M, S, p[q].x, p[q].y);
+    }
+    for (; t < n_tiles; t += CMB_G) {
       const float2 p = partial[int64_t(t) * N + n];
       lse_fold(M, S, p.x, p.y);
     }
