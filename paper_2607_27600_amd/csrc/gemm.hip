@@ -8,10 +8,9 @@
 //                      never leave registers.
 //
 // bf16 kernel: C[m][n] = sum_k A[m][k] B[n][k] with both operands K-contiguous, a 256x256
-// workgroup tile, 4 waves each owning a 128x128 sub-tile as 4x4 blocks of the 32x32x16
-// bf16 MFMA (fp32 accumulate), K staged 64 at a time through double-buffered LDS with a
-// padded row stride (144 B) so the 16-byte fragment reads of 8 consecutive rows hit
-// distinct banks.  For the LM head the vocabulary is the MFMA row (M) dimension, so each
+// workgroup tile, 8 waves (two per SIMD, so one wave's barrier and load waits hide behind
+// the other's MFMAs) each owning a 128x64 sub-tile as 4x2 blocks of the 32x32x16 bf16 MFMA
+// (fp32 accumulate), K staged 64 at a time through two LDS stages.  For the LM head the vocabulary is the MFMA row (M) dimension, so each
 // lane holds 64 logits of one entry and the reduction over the vocabulary is mostly
 // in-lane.  Tiles are rasterised entry-tile-fastest so consecutive workgroups share one
 // LM-head tile.
@@ -22,9 +21,11 @@ namespace cc {
 namespace {
 
 constexpr int GBM = 256, GBN = 256, GBK = 64;
-constexpr int WGM = 2, WGN = 2, GNT = WGM * WGN * 64;
-constexpr int GTM = GBM / WGM, GTN = GBN / WGN;      // 128 x 128 per wave
-constexpr int GMB = GTM / 32, GNB = GTN / 32;        // 4 x 4 MFMA blocks
+constexpr int WGM = 2, WGN = 4, GNT = WGM * WGN * 64;   // 8 waves: two per SIMD
+constexpr int NWAVE = WGM * WGN;
+constexpr int LPW = 32 / NWAVE;   // 1 KB direct-load instructions per wave per operand tile
+constexpr int GTM = GBM / WGM, GTN = GBN / WGN;      // 128 x 64 per wave
+constexpr int GMB = GTM / 32, GNB = GTN / 32;        // 4 x 2 MFMA blocks
 
 struct GemmArgs {
   const u16* A;
@@ -298,11 +299,11 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   // wave w, load instruction j covers tile rows (8w + j) * 8 .. +8; rows past the matrix
   // edge are clamped to the last row (their products land in outputs the epilogues
   // discard), so the loop has no branches
-  const u16* ga[8];
-  const u16* gb[8];
+  const u16* ga[LPW];
+  const u16* gb[LPW];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int r = (wave * 8 + j) * 8 + (lane >> 3);
+  for (int j = 0; j < LPW; ++j) {
+    const int r = (wave * LPW + j) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ (r & 7);
     const int ra = min(m0 + r, g.M - 1);
     if constexpr (GATED) {
@@ -316,13 +317,13 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8;
   }
   auto issue = [&](u16* stage, int k0) {
-    u16* base = stage + wave * 8 * 512;
+    u16* base = stage + wave * LPW * 512;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < LPW; ++j)
       __builtin_amdgcn_global_load_lds((global_void*)(ga[j] + k0), (lds_void*)(base + j * 512),
                                        16, 0, 0);
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < LPW; ++j)
       __builtin_amdgcn_global_load_lds((global_void*)(gb[j] + k0),
                                        (lds_void*)(base + GBM * GBK + j * 512), 16, 0, 0);
   };
@@ -354,11 +355,11 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   // scheduling hint: one fragment read between consecutive MFMAs, then the rest
   auto interleave = [&]() {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < GMB + GNB; ++i) {
       __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
       __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, GMB * GNB - (GMB + GNB), 0);
     __builtin_amdgcn_sched_barrier(0);
   };
   const int nk = g.K / GBK;
