@@ -1,0 +1,72 @@
+"""Turn two rocprofv3 counter runs of `bench.py --pmc-driver` into HBM bytes per LM-head launch.
+
+    rocprofv3 --pmc FETCH_SIZE -d <dir_fetch> -o run --output-format csv -- python bench.py --pmc-driver
+    rocprofv3 --pmc WRITE_SIZE -d <dir_write> -o run --output-format csv -- python bench.py --pmc-driver
+    python -m paper_2607_27600_amd.pmc_summary <dir_fetch> <dir_write> profiles/lmhead_c2_traffic.json
+
+FETCH_SIZE / WRITE_SIZE are in KiB per dispatch.  The driver also copies 1 GiB device to
+device; each counter is scaled by (1 GiB / what it reads for that copy), so the figures are
+calibrated against a transfer of known size.  The record carries the sha256 of gemm.hip;
+bench.py reports the traffic only while the source matches.
+"""
+from __future__ import annotations
+
+import csv
+import hashlib
+import json
+import os
+import sys
+
+GIB_KIB = 1 << 20
+
+
+def _per_dispatch(path: str, counter: str) -> list:
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            key = r["Dispatch_Id"]
+            out.setdefault(key, [r["Kernel_Name"], 0.0])
+            out[key][1] += float(r["Counter_Value"])
+    return list(out.values())
+
+
+def _find(rows, pred):
+    hits = [v for name, v in rows if pred(name)]
+    if not hits:
+        raise SystemExit("kernel not found in counter file")
+    return hits
+
+
+def main(fetch_dir: str, write_dir: str, out: str) -> None:
+    f_rows = _per_dispatch(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
+    w_rows = _per_dispatch(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
+    is_lm = lambda n: "gemm_tn_bf16" in n and "EpiLse" in n
+    is_copy = lambda n: "copy" in n.lower() and "gemm" not in n and "compact" not in n
+    # the copy is the last dispatch of the driver; take the largest copy-like dispatch
+    f_copy = max(_find(f_rows, is_copy))
+    w_copy = max(_find(w_rows, is_copy))
+    f_lm = _find(f_rows, is_lm)[-1]
+    w_lm = _find(w_rows, is_lm)[-1]
+    kf, kw = GIB_KIB / f_copy, GIB_KIB / w_copy
+    here = os.path.dirname(os.path.abspath(__file__))
+    with open(os.path.join(here, "csrc", "gemm.hip"), "rb") as fh:
+        digest = hashlib.sha256(fh.read()).hexdigest()
+    rec = {
+        "kernel": "gemm_tn_bf16<EpiLse> (LM head + fused log-sum-exp), C2 shapes",
+        "fetch_kib_raw": f_lm, "write_kib_raw": w_lm,
+        "copy_fetch_kib_raw": f_copy, "copy_write_kib_raw": w_copy,
+        "fetch_scale": kf, "write_scale": kw,
+        "bytes_per_launch": (f_lm * kf + w_lm * kw) * 1024.0,
+        "algorithmic_bytes": "W_lm 128256x4096 bf16 (1.05 GB) + U 4096x4096 bf16 (33.6 MB) read, "
+                             "partials 501x4096x8 B (16.4 MB) written",
+        "gemm_source_sha256": digest,
+    }
+    with open(out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+if __name__ == "__main__":
+    main(*sys.argv[1:4])
