@@ -279,8 +279,11 @@ constexpr int STAGE = (GBM + GBN) * GBK;   // bf16 elements per LDS stage (64 KB
 // The main loop.  Operand tiles go from global memory straight into LDS
 // (global_load_lds_dwordx4: lane i of a wave instruction fills bytes 16i..16i+15 of a 1 KB
 // run), so no registers stage them and no LDS write instructions are issued.  Tiles are
-// unpadded [rows][64] bf16 with the 16-byte chunk c of row r stored at chunk c ^ (r & 7):
-// the MFMA fragment reads of 8 consecutive rows then hit 8 distinct bank groups.  Two
+// unpadded [rows][64] bf16 with the 16-byte chunk c of row r stored at chunk
+// c ^ ((r >> 1) & 7).  The LDS serves a 16-byte read for 16 lanes at a time across 64
+// banks (256 B); the fragment reads of 16 consecutive rows at one chunk then cover all 64
+// banks exactly once (two 128-byte rows per bank cycle, the XOR spreading the 8 even and
+// the 8 odd rows over the 8 chunk slots).  Two
 // stages are distinct LDS objects so the compiler can tell the stage being filled from the
 // stage being read (a shared object would make it wait for the loads before every read).
 // One barrier per k-tile, placed after the step-3 fragments are read: past it, the next
@@ -304,7 +307,7 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     const int r = (wave * LPW + j) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ (r & 7);
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
     const int ra = min(m0 + r, g.M - 1);
     if constexpr (GATED) {
       // rows [64i, 64i+32) are W_gate rows [32i, 32i+32), rows [64i+32, 64i+64) the same
@@ -333,12 +336,12 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
 #pragma unroll
     for (int mb = 0; mb < GMB; ++mb) {
       const int r = wm * GTM + mb * 32 + col;
-      fa[mb] = as_bf16x8(ld16(As + r * GBK + ((c ^ (r & 7)) * 8)));
+      fa[mb] = as_bf16x8(ld16(As + r * GBK + ((c ^ ((r >> 1) & 7)) * 8)));
     }
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
       const int r = wn * GTN + nb * 32 + col;
-      fb[nb] = as_bf16x8(ld16(Bs + r * GBK + ((c ^ (r & 7)) * 8)));
+      fb[nb] = as_bf16x8(ld16(Bs + r * GBK + ((c ^ ((r >> 1) & 7)) * 8)));
     }
   };
   f32x16 acc[GMB][GNB];
