@@ -12,9 +12,9 @@
 //   Key tiles entirely at or before the block's first row are never visited (they are
 //   masked for every row), so the work per block shrinks towards the end of the
 //   sequence; only tiles that straddle the diagonal or the sequence end are masked.
-//   K tiles are stored row-major in LDS, V tiles transposed with the key order permuted
-//   to match the MFMA k-slots of the P operand; both are double buffered with one
-//   barrier per tile.
+//   K and V tiles go from global memory straight into LDS (no register staging), both
+//   row-major with XOR-swizzled 16-byte chunks; the V^T operand of the second product is
+//   read with LDS transpose reads.  Both are double buffered with one barrier per tile.
 // fp32 path: one thread per row, K/V tiles staged in LDS, exact fp32 online softmax.
 #include <type_traits>
 
@@ -23,21 +23,18 @@
 namespace cc {
 namespace {
 
-#define SCHED_VALU 0x002
-#define SCHED_MFMA 0x008
-#define SCHED_DS_READ 0x100
-#define SCHED_TRANS 0x400
-
 constexpr int BN = 64;            // keys per tile
 constexpr int HD = 128;           // head dim of the MFMA path
 constexpr int ROWS_W = 32;        // rows per wave
 constexpr int NWAVES = 4;
 constexpr int ROWS = ROWS_W * NWAVES;
-constexpr int KS = HD + 8;        // LDS row stride of K (elements): 272 B
-constexpr int VS = BN + 8;        // LDS row stride of V^T (elements): 144 B
-constexpr int K_TILE = BN * KS;
-constexpr int V_TILE = HD * VS;
+constexpr int TILE = BN * HD;     // elements of one K or V tile in LDS (16 KB, unpadded)
 constexpr float kRescale = 8.f;   // log2 headroom before the softmax reference max moves
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_void;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
 
 struct AttnArgs {
   const u16* q;
@@ -53,13 +50,38 @@ struct AttnArgs {
 
 __device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<const uint4*>(p); }
 
+// ds_read_b64_tr_b16: in each group of 16 lanes, lane i receives element i%4 of the 8-byte
+// chunks addressed by lanes i/4, 4 + i/4, 8 + i/4 and 12 + i/4 of its group.  With lane
+// 4e + c of a group addressing row r0 + e, columns c0 + 4c .. +3 of a row-major tile, lane i
+// gets column c0 + i of rows r0 .. r0+3: a transposed 4x16 block.
+__device__ __forceinline__ v4i16 ds_read_tr(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
+}
+
+// A wave-uniform pointer held in scalar registers, so that pointer + 32-bit lane offset
+// selects the scalar-base form of the load (no per-lane 64-bit address arithmetic).
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+  return reinterpret_cast<const char*>((uint64_t(hi) << 32) | lo);
+}
+
+// Per-slab page numbers of one tile (paged caches): slab i = keys 64t + 16i .. +15, which
+// lie in one page because pages hold a power of two >= 16 keys.  Indices past the
+// sequence's last page are clamped (such tiles take the per-lane path anyway).
+struct SlabPages {
+  int p[4];
+};
+
 template <bool PAGED>
 __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
-  // K tiles run one tile ahead of V tiles: while the softmax of tile t runs on the VALU, the
-  // MFMAs of S for tile t+1 are already issued, so each wave overlaps its own softmax with
-  // matrix work.  Two K buffers (tiles t+1, t+2) and two V buffers (tiles t, t+1).
-  __shared__ __attribute__((aligned(16))) u16 kl[2][K_TILE];
-  __shared__ __attribute__((aligned(16))) u16 vl[2][V_TILE];
+  // Two K and two V buffers as distinct objects: the compiler can then tell the buffer a
+  // DMA is filling from the one being read, and waits for the DMA only where asked.
+  __shared__ __attribute__((aligned(1024))) u16 kl0[TILE];
+  __shared__ __attribute__((aligned(1024))) u16 kl1[TILE];
+  __shared__ __attribute__((aligned(1024))) u16 vl0[TILE];
+  __shared__ __attribute__((aligned(1024))) u16 vl1[TILE];
 
   const int4 w = a.work[blockIdx.x];
   const int b = w.x, kvh = w.y, rb = w.z;
@@ -111,106 +133,117 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const int tm0 = min(te, max(tb, (pos_hi_wg + 1 + BN - 1) / BN));
   const int tm1 = (n % BN == 0) ? te : te - 1;
 
-  const u16* kbase = reinterpret_cast<const u16*>(a.k.base);
-  const u16* vbase = reinterpret_cast<const u16*>(a.v.base);
-
-  // global -> register staging
-  // K: thread owns 16-byte column chunk kc of rows kr0 + 16*i.
-  const int kc = tid & 15, kr0 = tid >> 4;
-  // V: thread owns keys 4*vg .. 4*vg+3, dims 8*vd .. 8*vd+7.
-  const int vg = tid & 15, vd = tid >> 4;
-  uint4 kreg[4], vreg[4];
-
-  // Row addressing.  Contiguous caches: this thread's rows of tile 0 are fixed pointers
-  // and a tile is a uniform (scalar) offset, so full tiles cost one add per row; only the
-  // last, partial tile clamps rows to n-1.  Paged caches: one block-table lookup per row.
-  const u16* kp[4];
-  const u16* vp[4];
-  if constexpr (!PAGED) {
-    const u16* kplane = kbase + kv_off<false>(a.k, b, a.layer, kvh, 0);
-    const u16* vplane = vbase + kv_off<false>(a.v, b, a.layer, kvh, 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      kp[i] = kplane + int64_t(kr0 + 16 * i) * a.k.tok_stride + kc * 8;
-      vp[i] = vplane + int64_t(4 * vg + i) * a.v.tok_stride + vd * 8;
-    }
-  }
-  auto load_k = [&](int t) {
-    const int key0 = t * BN;   // rows past n are clamped to n-1 and masked
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        kreg[i] = ld16(kbase + kv_off<true>(a.k, b, a.layer, kvh, min(key0 + kr0 + 16 * i, n - 1)) +
-                       kc * 8);
-    } else {
-      if (key0 + BN <= n) {
-        const int64_t off = int64_t(key0) * a.k.tok_stride;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) kreg[i] = ld16(kp[i] + off);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = min(key0 + kr0 + 16 * i, n - 1);
-          kreg[i] = ld16(kp[i] + (int64_t(key - kr0 - 16 * i) * a.k.tok_stride));
-        }
-      }
-    }
-  };
-  auto load_v = [&](int t) {
-    const int key0 = t * BN;
-    if constexpr (PAGED) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = key0 + 4 * vg + i;
-        // value rows past n get zero (their weights are 0, but garbage could be NaN)
-        vreg[i] = key < n ? ld16(vbase + kv_off<true>(a.v, b, a.layer, kvh, key) + vd * 8)
-                          : make_uint4(0, 0, 0, 0);
-      }
-    } else {
-      const int64_t off = int64_t(key0) * a.v.tok_stride;
-      if (key0 + BN <= n) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) vreg[i] = ld16(vp[i] + off);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          vreg[i] = key0 + 4 * vg + i < n ? ld16(vp[i] + off) : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  // position of key 4*vg within the permuted V^T row (see the PV operand layout below)
-  const int vpos = (vg >> 2) * 16 + (vg & 1) * 8 + ((vg >> 1) & 1) * 4;
-  auto store_k = [&](u16* Kl) {
+  // ---- tile DMA (global -> LDS, no registers).  Wave w, instruction i fills tile rows
+  // 16i + 4w .. +3 (1 KB): lane l writes row 16i + 4w + l/16 at 16-byte position l%16, and
+  // loads the row's chunk (l%16) ^ swz(row) there, swz = row & 15 for K and
+  // (row & 3) << 2 for V.  Rows past the sequence end are clamped to its last key (their
+  // weights are 0 and the clamped data is finite).
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int drow = 4 * wave + (lane >> 4);
+  const int kch = (lane & 15) ^ (drow & 15);
+  const int vch = (lane & 15) ^ ((drow & 3) << 2);
+  const char* kbase = reinterpret_cast<const char*>(a.k.base);
+  const char* vbase = reinterpret_cast<const char*>(a.v.base);
+  const int64_t kts = a.k.tok_stride * 2, vts = a.v.tok_stride * 2;   // bytes per key
+  uint32_t klane = uint32_t(drow * kts + kch * 16);
+  uint32_t vlane = uint32_t(drow * vts + vch * 16);
+  // contiguous caches: the (sequence, layer, head) plane; paged: layer + head part
+  const char* kplane = kbase + (PAGED ? int64_t(a.layer) * a.k.layer_stride + int64_t(kvh) * a.k.head_stride
+                                      : kv_off<false>(a.k, b, a.layer, kvh, 0)) * 2;
+  const char* vplane = vbase + (PAGED ? int64_t(a.layer) * a.v.layer_stride + int64_t(kvh) * a.v.head_stride
+                                      : kv_off<false>(a.v, b, a.layer, kvh, 0)) * 2;
+  const int32_t* btab = PAGED ? a.k.block_table + int64_t(b) * a.k.max_pages : nullptr;
+  const int last_page = PAGED ? (n - 1) >> a.k.page_shift : 0;
+  auto pages_of = [&](int t) {
+    SlabPages s;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<uint4*>(Kl + (kr0 + 16 * i) * KS + kc * 8) = kreg[i];
+      s.p[i] = PAGED ? btab[min((t * BN + 16 * i) >> a.k.page_shift, last_page)] : 0;
+    return s;
   };
-  auto store_v = [&](u16* Vl) {
-    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-    const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-    const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
+  // Fill an LDS tile with tile t.  Full tiles: a uniform base per slab plus the lane's fixed
+  // offset.  The last, partial tile: per-lane rows (clamped), per-lane page lookups.
+  auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, uint32_t lane_off,
+                   int ch, int64_t ts, const SlabPages& pg) {
+    const int key0 = t * BN;
+    u16* lds = dst + wave_u * 4 * HD;
+    if (key0 + BN <= n) {
+      // keep the 32-bit offset opaque here so that it is not widened outside the loop
+      asm volatile("" : "+v"(lane_off));
 #pragma unroll
-    for (int wd = 0; wd < 4; ++wd) {
-      // dims 8*vd + 2*wd (low halves) and 8*vd + 2*wd + 1 (high halves)
-      uint2 lo, hi2;
-      lo.x = (r0[wd] & 0xffffu) | (r1[wd] << 16);
-      lo.y = (r2[wd] & 0xffffu) | (r3[wd] << 16);
-      hi2.x = (r0[wd] >> 16) | (r1[wd] & 0xffff0000u);
-      hi2.y = (r2[wd] >> 16) | (r3[wd] & 0xffff0000u);
-      const int d0 = vd * 8 + 2 * wd;
-      *reinterpret_cast<uint2*>(Vl + d0 * VS + vpos) = lo;
-      *reinterpret_cast<uint2*>(Vl + (d0 + 1) * VS + vpos) = hi2;
+      for (int i = 0; i < 4; ++i) {
+        int64_t slab;
+        if constexpr (PAGED)
+          slab = int64_t(pg.p[i]) * kv.page_stride + int64_t((key0 + 16 * i) & kv.page_mask) * kv.tok_stride;
+        else
+          slab = int64_t(key0 + 16 * i) * kv.tok_stride;
+        const char* base = uniform_ptr(plane + slab * 2);
+        __builtin_amdgcn_global_load_lds((global_void*)(base + lane_off),
+                                         (lds_void*)(lds + i * 16 * HD), 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = min(key0 + 16 * i + drow, n - 1);
+        int64_t off;
+        if constexpr (PAGED)
+          off = int64_t(btab[key >> kv.page_shift]) * kv.page_stride + int64_t(key & kv.page_mask) * kv.tok_stride;
+        else
+          off = int64_t(key) * kv.tok_stride;
+        __builtin_amdgcn_global_load_lds((global_void*)(plane + off * 2 + ch * 16),
+                                         (lds_void*)(lds + i * 16 * HD), 16, 0, 0);
+      }
     }
   };
 
-  // S^T[key][row] for the 64 keys of a tile: two 32-key blocks; 16 MFMAs, MFMA j uses
-  // key block j%2 and dims 16*(j/2) ..
+  // ---- fragment reads.  K (A operand of S^T = K Q^T): MFMA j reads row (j&1)*32 + col,
+  // chunk 2*(j>>1) + hi.  V^T (A operand of O^T = V^T P^T): MFMA j = (k-step kk, d block db)
+  // needs d = 32 db + col and keys 16kk + 4hi + {0..3}, 16kk + 8 + 4hi + {0..3} (the order
+  // of the P operand's k-slots): two transpose reads of 4 keys x 16 dims.
+  uint32_t koff[8];
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) koff[jj] = col * 256 + 16 * ((2 * jj + hi) ^ (col & 15));
+  uint32_t voff[4];
+  {
+    const int G = lane >> 4, L = lane & 15, y = L >> 2;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+      voff[db] = (4 * (G >> 1) + y) * 256 + 64 * (db ^ y) + 32 * (G & 1) + 8 * (L & 3);
+  }
   auto kfrag = [&](const u16* Kl, int j) {
-    return as_bf16x8(ld16(Kl + ((j & 1) * 32 + col) * KS + (j >> 1) * 16 + hi * 8));
+    return as_bf16x8(*reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(Kl) +
+                                                     koff[j >> 1] + (j & 1) * 8192));
   };
-  auto vfrag = [&](const u16* Vl, int j) {   // PV MFMA j: k-step j/4, d block j%4
-    return as_bf16x8(ld16(Vl + ((j & 3) * 32 + col) * VS + (j >> 2) * 16 + hi * 8));
+  auto vfrag = [&](const u16* Vl, int j) {
+    const char* p = reinterpret_cast<const char*>(Vl) + voff[j & 3] + (j >> 2) * 4096;
+    const v4i16 lo = ds_read_tr(p), hi2 = ds_read_tr(p + 2048);
+    const v8i16 both = __builtin_shufflevector(lo, hi2, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, both);
+  };
+
+  // max over both lane halves (they hold the two 32-key blocks of one row)
+  auto half_max = [](float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  };
+  auto row_max = [&](const f32x16(&s)[2]) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, s[mb][e]);
+    return half_max(m);
+  };
+  auto apply_mask = [&](f32x16(&s)[2], int t) {
+    const int key0 = t * BN;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = key0 + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
+        const bool ok = key < n && (a.inclusive ? key >= pos : key > pos);
+        s[mb][e] = ok ? s[mb][e] : -INFINITY;
+      }
   };
 
   float m_run = -INFINITY, l_run = 0.f;
@@ -218,54 +251,55 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
 #pragma unroll
   for (int db = 0; db < 4; ++db) acc[db] = f32x16{};
 
-  // prologue: K(tb), V(tb) and K(tb+1) in LDS, S(tb) in registers
-  load_k(tb);
-  load_v(tb);
-  store_k(kl[0]);
-  store_v(vl[0]);
-  load_k(min(tb + 1, te - 1));
-  store_k(kl[1]);
+  // prologue: K(tb), V(tb), K(tb+1) in LDS; S(tb) and its unmasked row max in registers.
+  // Page numbers: pk for the K tile of the next step (t+2), pv for its V tile (t+1), pn
+  // for the K tile after (t+3), loaded one step ahead of use.
+  SlabPages pk = pages_of(min(tb + 2, te - 1));
+  SlabPages pv = pages_of(min(tb + 1, te - 1));
+  SlabPages pn = pages_of(min(tb + 3, te - 1));
+  {
+    const SlabPages p0 = pages_of(tb);
+    issue(kl0, tb, a.k, kplane, klane, kch, kts, p0);
+    issue(vl0, tb, a.v, vplane, vlane, vch, vts, p0);
+    issue(kl1, min(tb + 1, te - 1), a.k, kplane, klane, kch, kts, pv);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  f32x16 s_cur[2], s_nxt[2];
-  s_cur[0] = f32x16{};
-  s_cur[1] = f32x16{};
+  f32x16 sa[2], sb[2];
+  sa[0] = f32x16{};
+  sa[1] = f32x16{};
 #pragma unroll
-  for (int j = 0; j < 16; ++j) s_cur[j & 1] = mfma32(kfrag(kl[0], j), qf[j >> 1], s_cur[j & 1]);
+  for (int j = 0; j < 16; ++j) sa[j & 1] = mfma32(kfrag(kl0, j), qf[j >> 1], sa[j & 1]);
+  float mx = row_max(sa);
 
-  // One tile.  S(t) is in s_cur; K(t+1) sits in kl[(t+1-tb)&1] and V(t) in vl[(t-tb)&1]; the
-  // loads of K(t+2), V(t+1) refill the buffers freed by K(t), V(t-1).  The step is written
-  // in the order it should issue (sched_barrier fences keep the compiler from regrouping):
-  // the 16 MFMAs of S(t+1) are spread over the exponentials of this tile's softmax, and the
-  // 16 MFMAs of P V over the LDS stores of the next tiles.  Past the last tile, loads and
-  // S are clamped to the last tile and land in buffers nobody reads.
-  auto step = [&](int t, auto mask_tag) {
-    constexpr bool kMask = decltype(mask_tag)::value;
-    const int i = t - tb;
-    const u16* Kn = kl[(i + 1) & 1];
-    const u16* Vc = vl[i & 1];
-    load_k(min(t + 2, te - 1));
-    load_v(min(t + 1, te - 1));
+  // Tile t with parity P = (t - tb) & 1.  S(t) is in sc with its unmasked row max in mx;
+  // K(t+1) in kl[1-P], V(t) in vl[P].  The DMAs of K(t+2) -> kl[P] and V(t+1) -> vl[1-P]
+  // refill buffers freed by the previous tile.  Issue order: the 16 MFMAs of S(t+1) carry
+  // the exponentials of tile t; the 16 MFMAs of P V carry the bf16 packing of P, the row
+  // sums and the row max of S(t+1).  sched_barrier fences keep the compiler from regrouping.
+  auto step = [&](int t, auto par, bool masked) {
+    constexpr int P = decltype(par)::value;
+    f32x16(&sc)[2] = P ? sb : sa;
+    f32x16(&sn)[2] = P ? sa : sb;
+    const u16* Kn = P ? kl0 : kl1;
+    u16* Kfree = P ? kl1 : kl0;
+    const u16* Vc = P ? vl1 : vl0;
+    u16* Vfree = P ? vl0 : vl1;
+    issue(Kfree, min(t + 2, te - 1), a.k, kplane, klane, kch, kts, pk);
+    issue(Vfree, min(t + 1, te - 1), a.v, vplane, vlane, vch, vts, pv);
+    if constexpr (PAGED) {
+      pv = pk;
+      pk = pn;
+      pn = pages_of(min(t + 4, te - 1));
+    }
     bf16x8 kf[4];
     kf[0] = kfrag(Kn, 0);
     kf[1] = kfrag(Kn, 1);
     kf[2] = kfrag(Kn, 2);
-    if (kMask) {
-      const int key0 = t * BN;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = key0 + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-          const bool ok = key < n && (a.inclusive ? key >= pos : key > pos);
-          s_cur[mb][e] = ok ? s_cur[mb][e] : -INFINITY;
-        }
+    if (masked) {
+      apply_mask(sc, t);
+      mx = row_max(sc);
     }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s_cur[mb][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
     // Lazy rescaling: the reference max only moves when the row max grows by more than
     // 2^8 in probability units (or on the first non-empty tile).  Numerator and
     // denominator always share the reference, so the result is unchanged; p stays <= 256.
@@ -273,58 +307,79 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     const float corr = up ? fast_exp2((m_run - mx) * a.c2) : 1.f;   // 0 when m_run = -inf
     m_run = up ? mx : m_run;
     const float mc = (m_run == -INFINITY ? 0.f : m_run) * a.c2;
-    s_nxt[0] = f32x16{};
-    s_nxt[1] = f32x16{};
-    float lsum = 0.f;
+    sn[0] = f32x16{};
+    sn[1] = f32x16{};
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (j + 3 < 16) kf[(j + 3) & 3] = kfrag(Kn, j + 3);
-      s_nxt[j & 1] = mfma32(kf[j & 3], qf[j >> 1], s_nxt[j & 1]);
+      sn[j & 1] = mfma32(kf[j & 3], qf[j >> 1], sn[j & 1]);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int f = 2 * j + u, mb = f >> 4, e = f & 15;
-        const float p = fast_exp2(fmaf(s_cur[mb][e], a.c2, -mc));
+        const float p = fast_exp2(fmaf(sc[mb][e], a.c2, -mc));
         // pin the exponential here, between the MFMAs, instead of next to its later uses
         asm volatile("" ::"v"(p));
-        s_cur[mb][e] = p;
-        lsum += p;
+        sc[mb][e] = p;
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    l_run = l_run * corr + lsum;
-    // P^T operand: k-step kk covers keys 16*kk .. 16*kk+15; lane half hi holds keys
-    // {4hi..4hi+3, 8+4hi..8+4hi+3} of that step, i.e. S^T entries 8*(kk%2)..+7 of block kk/2
-    bf16x8 pf[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[kk][e] = (__bf16)s_cur[kk >> 1][(kk & 1) * 8 + e];
     if (__any(corr != 1.f)) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) acc[db] *= corr;
     }
+    // P^T operand: k-step kk covers keys 16kk .. 16kk+15; lane half hi holds keys
+    // {4hi..4hi+3, 8+4hi..8+4hi+3} of that step, i.e. S^T entries 8*(kk%2)..+7 of block kk/2
+    bf16x8 pf[4];
+    auto pack = [&](int kk) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[kk][e] = (__bf16)sc[kk >> 1][(kk & 1) * 8 + e];
+    };
     bf16x8 vf[4];
     vf[0] = vfrag(Vc, 0);
     vf[1] = vfrag(Vc, 1);
     vf[2] = vfrag(Vc, 2);
+    pack(0);
+    float ls0 = 0.f, ls1 = 0.f, m0 = -INFINITY, m1 = -INFINITY;
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (j + 3 < 16) vf[(j + 3) & 3] = vfrag(Vc, j + 3);
       acc[j & 3] = mfma32(vf[j & 3], pf[j >> 2], acc[j & 3]);
-      if (j == 7) store_k(kl[i & 1]);
-      if (j == 11) store_v(vl[(i + 1) & 1]);
+      if ((j & 3) == 3 && j < 15) pack((j >> 2) + 1);
+      ls0 += sc[j >> 3][(2 * j) & 15];
+      ls1 += sc[j >> 3][(2 * j + 1) & 15];
+      asm volatile("" : "+v"(ls0), "+v"(ls1));
+      if (j >= 2) {
+        // row max of S(t+1), whose MFMAs were issued during the exponentials: 32 entries
+        // over slots 2..12
+        const int f = j - 2;
+        if (f < 4) {
+          m0 = fmaxf(m0, fmaxf(sn[0][3 * f], fmaxf(sn[0][3 * f + 1], sn[0][3 * f + 2])));
+        } else if (f < 5) {
+          m0 = fmaxf(m0, fmaxf(sn[0][12], fmaxf(sn[0][13], sn[0][14])));
+          m1 = fmaxf(m1, sn[0][15]);
+        } else if (f < 10) {
+          const int e0 = 3 * (f - 5);
+          m1 = fmaxf(m1, fmaxf(sn[1][e0], fmaxf(sn[1][e0 + 1], sn[1][e0 + 2])));
+        } else if (f < 11) {
+          m1 = fmaxf(m1, sn[1][15]);
+        }
+        asm volatile("" : "+v"(m0), "+v"(m1));
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
-    s_cur[0] = s_nxt[0];
-    s_cur[1] = s_nxt[1];
+    l_run = l_run * corr + (ls0 + ls1);
+    mx = half_max(fmaxf(m0, m1));
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's DMAs have landed
+    __syncthreads();                 // everyone's, and everyone is done with K(t+1), V(t)
   };
-  int t = tb;
-  for (; t < tm0; ++t) step(t, std::true_type{});
-  for (; t < tm1; ++t) step(t, std::false_type{});
-  for (; t < te; ++t) step(t, std::true_type{});
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  for (int t = tb; t < te; t += 2) {
+    step(t, I0{}, t < tm0 || t >= tm1);
+    if (t + 1 < te) step(t + 1, I1{}, t + 1 < tm0 || t + 1 >= tm1);
+  }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
