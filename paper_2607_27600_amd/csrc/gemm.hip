@@ -268,7 +268,7 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 // Scheduling hints: interleave MFMAs with LDS reads / writes / global loads so the matrix
 // pipe stays busy while the wave issues its memory traffic.
 #define SCHED_MFMA 0x008
-#define SCHED_VMEM_READ 0x020
+#define SCHED_VMEM 0x010
 #define SCHED_DS_READ 0x100
 #define SCHED_DS_WRITE 0x200
 
@@ -288,6 +288,7 @@ constexpr int STAGE = (GBM + GBN) * GBK;   // bf16 elements per LDS stage (64 KB
 // stage being read (a shared object would make it wait for the loads before every read).
 // One barrier per k-tile, placed after the step-3 fragments are read: past it, the next
 // stage is complete and the current one is free for the loads of the tile after next.
+// Each stage is loaded in two halves issued between MFMAs (see the loop below).
 template <class Epi, bool GATED = false>
 __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   __shared__ __attribute__((aligned(1024))) u16 lds0[STAGE];
@@ -319,16 +320,13 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     }
     gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8;
   }
-  auto issue = [&](u16* stage, int k0) {
-    u16* base = stage + wave * LPW * 512;
+  // Half h of a stage: h = 0 the A rows, h = 1 the B rows (LPW direct loads per wave).
+  auto issue_half = [&](u16* stage, int k0, int h) {
+    u16* base = stage + wave * LPW * 512 + h * GBM * GBK;
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      __builtin_amdgcn_global_load_lds((global_void*)(ga[j] + k0), (lds_void*)(base + j * 512),
-                                       16, 0, 0);
-#pragma unroll
-    for (int j = 0; j < LPW; ++j)
-      __builtin_amdgcn_global_load_lds((global_void*)(gb[j] + k0),
-                                       (lds_void*)(base + GBM * GBK + j * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((global_void*)((h ? gb[j] : ga[j]) + k0),
+                                       (lds_void*)(base + j * 512), 16, 0, 0);
   };
   auto fread = [&](const u16* As, int ks, bf16x8 (&fa)[GMB], bf16x8 (&fb)[GNB]) {
     const u16* Bs = As + GBM * GBK;
@@ -365,14 +363,30 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, GMB * GNB - (GMB + GNB), 0);
     __builtin_amdgcn_sched_barrier(0);
   };
+  // the same, with one direct load after every other MFMA
+  auto interleave_loads = [&]() {
+#pragma unroll
+    for (int i = 0; i < GMB * GNB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      if (i < GMB + GNB) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+      if ((i & 1) == 0) __builtin_amdgcn_sched_group_barrier(SCHED_VMEM, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
   const int nk = g.K / GBK;
   bf16x8 fa0[GMB], fb0[GNB], fa1[GMB], fb1[GNB];
-  // one k-tile from `cur`; fragments of each step are read during the previous step
+  // One k-tile from `cur`; fragments of each step are read during the previous step.  The
+  // loads of a stage are split in two halves issued between MFMAs, never in one burst: when
+  // every wave of the CU issues its loads at once they queue on the memory pipeline and the
+  // waves stall behind them.  The B half of `nxt` (k-tile kt+1) goes out during the first
+  // step; the A half of `cur` (k-tile kt+2, past the end: a reload) right after the barrier
+  // that frees `cur`.
   auto tile = [&](const u16* cur, u16* nxt, int kt) {
     __builtin_amdgcn_sched_barrier(0);
     fread(cur, 1, fa1, fb1);
     mfmas(fa0, fb0);
-    interleave();
+    issue_half(nxt, min(kt + 1, nk - 1) * GBK, 1);
+    interleave_loads();
     fread(cur, 2, fa0, fb0);
     mfmas(fa1, fb1);
     interleave();
@@ -381,13 +395,14 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     interleave();
     __builtin_amdgcn_s_waitcnt(0);   // this wave's loads into `nxt` have landed
     __syncthreads();                 // everyone's have, and everyone is done with `cur`
-    issue(const_cast<u16*>(cur), min(kt + 2, nk - 1) * GBK);   // past the end: a reload
+    issue_half(const_cast<u16*>(cur), min(kt + 2, nk - 1) * GBK, 0);
     fread(nxt, 0, fa0, fb0);
     mfmas(fa1, fb1);
-    interleave();
+    interleave_loads();
   };
-  issue(lds0, 0);
-  issue(lds1, min(1, nk - 1) * GBK);
+  issue_half(lds0, 0, 0);
+  issue_half(lds0, 0, 1);
+  issue_half(lds1, min(1, nk - 1) * GBK, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   fread(lds0, 0, fa0, fb0);
