@@ -98,6 +98,126 @@ def lmhead_traffic():
     return rec.get("bytes_per_launch") if rec.get("gemm_source_sha256") == digest else None
 
 
+def flushed_ms(fn, reps: int, flush) -> float:
+    """Mean time of fn() on the current stream with the 256 MB Infinity Cache and the L2s
+    flushed before every call (a 1 GiB buffer is rewritten in between)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        flush.add_(1)
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return sum(a.elapsed_time(b) for a, b in ev) / reps
+
+
+def select_sweep(dev, flush, reps: int = 5) -> dict:
+    """Keep selection at a size where it streams from HBM: 4096 segments of 32768 scores
+    (512 MB), keep 25% of each.  Scores are drawn like surprisals (exponential, mean 3)."""
+    import torch
+    from paper_2607_27600_amd import cc
+    n_segs, seg, k = 4096, 32768, 8192
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    scores = torch.empty(n_segs * seg, dtype=torch.float32, device=dev).exponential_(1 / 3.0, generator=g)
+    keep = torch.empty(n_segs * k, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(1, cc.cc_select_workspace(n_segs)), dtype=torch.uint8, device=dev)
+    starts = [i * seg for i in range(n_segs)]
+    lens = [seg] * n_segs
+    ks = [k] * n_segs
+    cc.cc_select_keep(scores, starts, lens, ks, keep, ws)
+    ms = flushed_ms(lambda: cc.cc_select_keep(scores, starts, lens, ks, keep, ws), reps, flush)
+    nbytes = 4 * n_segs * seg + 4 * n_segs * k
+    del scores, keep
+    return {"segments": n_segs, "segment_len": seg, "k": k, "ms": ms, "bytes": nbytes,
+            "gb_s": nbytes / (ms * 1e-3) / 1e9, "frac_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "note": "Infinity Cache flushed before each call; bytes = scores read + keep written"}
+
+
+def bench_generic(args, cfg, dev) -> dict:
+    """Whole refreshes of any configuration: cc_score, keep selection, in-place compaction of
+    every cache layer (paged caches compact within each sequence's own pages)."""
+    import torch
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    t_gen = time.perf_counter()
+    w = Workload(cfg, device=dev)
+    t_gen = time.perf_counter() - t_gen
+    p = w.problem
+    N, L, hkv, d = cfg.n_tokens, w.cache_layers, cfg.n_heads_kv, cfg.head_dim
+    cu = cfg.cu_seqlens
+    per_head = int(cfg.per_head_select)
+    starts, lens, ks = [], [], []
+    for b in range(cfg.n_seqs):
+        for _ in range(hkv if per_head else 1):
+            starts.append(int(cu[b]))
+            lens.append(int(cu[b + 1] - cu[b]))
+            ks.append(int(cfg.keep[b]))
+    scores = torch.empty(N, dtype=torch.float32, device=dev)
+    keep = torch.empty(sum(ks), dtype=torch.int32, device=dev)
+    ws_score = torch.empty(max(1, cc.cc_score_workspace(p)), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(max(1, cc.cc_select_workspace(len(ks))), dtype=torch.uint8, device=dev)
+    ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, per_head)), dtype=torch.uint8, device=dev)
+    inp = w.inputs()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        cc.cc_score(p, inp, scores, ws_score)
+        mark(1)
+        cc.cc_select_keep(scores, starts, lens, ks, keep, ws_sel)
+        mark(2)
+        cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp)
+        mark(3)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    names = ["score", "select", "compact_in_place"]
+    part = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(names)}
+    kept_rows = sum(ks) if per_head else sum(ks) * hkv            # (token, head) rows per layer
+    moved = 2 * (2 * L * kept_rows * d * 2)                       # K and V, read + write
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    cmp_flushed = flushed_ms(lambda: cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp),
+                             5, flush)
+    hq, D, V = cfg.n_heads_q, cfg.hidden, cfg.vocab
+    att_flop = 2.0 * d * hq * sum(n * (n - 1) for n in cfg.seq_lens)
+    lm_flop = 2.0 * N * D * V
+    if cfg.mode == "full":
+        per_layer = 2.0 * N * D * (hq * d) * 2 + 2.0 * N * D * cfg.ffn * 3
+        score_flop = cfg.n_layers * (per_layer + att_flop) + lm_flop
+    else:
+        score_flop = att_flop + 2.0 * N * D * hq * d + lm_flop
+    return {
+        "metric": METRIC, "value": N / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "n_cached": N, "n_seqs": cfg.n_seqs,
+                   "cache_layers": L, "paged": bool(cfg.paged), "mode": cfg.mode},
+        "breakdown_ms": part,
+        "score_tflops": score_flop / (part["score"] * 1e-3) / 1e12,
+        "compact": {"bytes_moved": moved, "ms": part["compact_in_place"],
+                    "gb_s": moved / (part["compact_in_place"] * 1e-3) / 1e9,
+                    "ms_cache_flushed": cmp_flushed,
+                    "gb_s_cache_flushed": moved / (cmp_flushed * 1e-3) / 1e9,
+                    "frac_hbm_cache_flushed": moved / (cmp_flushed * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "input_generation_s": t_gen,
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -113,9 +233,11 @@ def main():
     from synth import configs as C
 
     cfg = C.CONFIGS[args.config]
-    assert cfg.mode == "last_layer" and not cfg.paged and cfg.n_seqs == 1, \
-        "bench.py times the single-sequence fast-path workloads"
     dev = torch.device("cuda:0")
+    if not (cfg.mode == "last_layer" and not cfg.paged and cfg.n_seqs == 1):
+        torch.cuda.set_device(dev)
+        print(json.dumps(bench_generic(args, cfg, dev)), flush=True)
+        return
     torch.cuda.set_device(dev)
     t_gen = time.perf_counter()
     w = Workload(cfg, device=dev, keep_host=not args.no_cpu_baseline)
@@ -205,6 +327,13 @@ def main():
     torch.cuda.synchronize()
     ip_ms = ev_ip[0].elapsed_time(ev_ip[1]) / args.steps
 
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    ip_flushed = flushed_ms(lambda: cc.cc_compact_kv(p, w.kv, keep, ks, int(cfg.per_head_select),
+                                                     workspace=ws_cmp), 5, flush)
+    del out_k, out_v
+    sweep = select_sweep(dev, flush)
+    del flush
+
     att_flop = 2.0 * d * Hq * sum(n * (n - 1) for n in cfg.seq_lens)
     lm_flop = 2.0 * N * D * V
     wo_flop = 2.0 * N * D * Hq * d
@@ -239,7 +368,11 @@ def main():
         "compact": {"gb_s": compact_gbs, "frac_hbm": compact_gbs / PEAK_HBM_GBS,
                     "bytes_moved": 2 * kept_bytes, "mode": "out of place, 32-layer cache"},
         "compact_in_place": {"ms": ip_ms, "gb_s": 2 * kept_bytes / (ip_ms * 1e-3) / 1e9,
-                             "frac_hbm": 2 * kept_bytes / (ip_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
+                             "frac_hbm": 2 * kept_bytes / (ip_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                             "ms_cache_flushed": ip_flushed,
+                             "gb_s_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9,
+                             "frac_hbm_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9 / PEAK_HBM_GBS},
+        "select_sweep": sweep,
         "breakdown_ms": part_ms,
         "wo_proj_tflops": wo_flop / (part_ms["wo_proj"] * 1e-3) / 1e12,
         "input_generation_s": t_gen,

@@ -44,6 +44,53 @@ def test_select_matches_oracle_with_ties(seed):
             off += k
 
 
+@pytest.mark.parametrize("lens", [[32769, 40000, 70001], [5, 32768, 33000]])
+def test_select_long_segments(lens):
+    """Segments longer than the register-resident path holds go through the kernel that
+    re-reads the scores at every pass (any segment past 32768 in the launch selects it)."""
+    print(f"[select] long lens={lens}", flush=True)
+    r = np.random.default_rng(len(lens) + lens[0])
+    total = sum(lens)
+    pool = np.array([-0.0, 0.0, 1.5, 2.0, np.inf, -np.inf, np.nan], dtype=np.float32)
+    s = np.where(r.random(total) < 0.3, pool[r.integers(0, len(pool), total)],
+                 r.standard_normal(total).astype(np.float32)).astype(np.float32)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    for kfrac in (0.2, 0.5):
+        ks = [max(1, int(kfrac * n)) for n in lens]
+        got = _gpu_select(s, starts, lens, ks)
+        off = 0
+        for st, n, k in zip(starts, lens, ks):
+            np.testing.assert_array_equal(got[off:off + k], O.select_keep(s[st:st + n], k),
+                                          err_msg=f"len={n} k={k}")
+            off += k
+
+
+def test_select_score_ranges():
+    """Distributions that stress the radix passes on min-relative keys: surprisal-like
+    (exponential), a narrow band (few bits of range), huge magnitudes of both signs, and
+    scores one ulp apart; segment starts not 16-byte aligned."""
+    r = np.random.default_rng(21)
+    n = 9001
+    base = np.float32(11.76)
+    segs = [
+        r.exponential(3.0, n).astype(np.float32),
+        (base + r.standard_normal(n) * 1e-3).astype(np.float32),
+        (r.uniform(-1, 1, n) * 3e38).astype(np.float32),
+        np.nextafter(np.full(n, base), np.float32(np.inf)) * (r.random(n) < 0.5) + base * (r.random(n) >= 0.5),
+        r.standard_normal(n).astype(np.float32),
+    ]
+    segs[3] = segs[3].astype(np.float32)
+    segs[4][::7] = -np.inf
+    segs[4][::11] = np.inf
+    s = np.concatenate([np.zeros(3, np.float32)] + segs).astype(np.float32)
+    starts = [3 + i * n for i in range(len(segs))]
+    for k in (1, 17, n // 4, n - 1):
+        got = _gpu_select(s, starts, [n] * len(segs), [k] * len(segs))
+        for i, st in enumerate(starts):
+            np.testing.assert_array_equal(got[i * k:(i + 1) * k], O.select_keep(s[st:st + n], k),
+                                          err_msg=f"segment {i} k={k}")
+
+
 def test_select_overlapping_segments_identical_lists():
     r = np.random.default_rng(9)
     s = r.standard_normal(4096).astype(np.float32)
