@@ -100,3 +100,26 @@ def test_c5_full_size_paged_sampled_rows():
     rows = C.sample_rows(C.C5, count=64)
     got, ref, _ = _run(C.C5, rows=rows)
     _check(got, ref, "bf16")
+
+
+def test_bf16_outlier_key_channels():
+    """Stress variant: four key channels scaled by 16 (the outlier channels real caches
+    have), so logits span a much wider range and the softmax reference moves often."""
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.shrink(C.C2, seq_lens=(1000,), cache_layers=1)
+    print("[attention] outlier key channels, n=1000", flush=True)
+    w = Workload(cfg, cache_layers=1, keep_host=True, with_lm_head=False)
+    ch = [3, 40, 77, 120]
+    w.k_cache[..., ch] = w.k_cache[..., ch] * 16          # exact in bf16 (power of two)
+    hk = (w.host["k"].astype(np.uint32) << 16).view(np.float32).copy()
+    hk[..., ch] *= 16
+    hk16 = (hk.view(np.uint32) >> 16).astype(np.uint16)
+    p = cc.problem(dtype=cfg.dtype, cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=cfg.n_heads_q,
+                   n_heads_kv=cfg.n_heads_kv, head_dim=cfg.head_dim, hidden=cfg.hidden,
+                   vocab=cfg.vocab)
+    o = torch.full_like(w.q, float("nan"))
+    cc.cc_attention_cc(p, w.q, w.kv, 0, o)
+    torch.cuda.synchronize()
+    ref = O.attention_cc(w.host["q"], hk16, w.host["v"], "strict")
+    _check(f64(o), ref, "bf16")
