@@ -211,6 +211,42 @@ def silu(x):
     return x / (1.0 + np.exp(-x))
 
 
+def _layer(h, W, K, V, rows, seq, pos, cu, n_heads_q, head_dim, theta, eps, diag, scale):
+    """One pre-norm transformer layer for the requested rows with fresh queries against
+    the stored keys/values K, V ([Hkv][N][d], already rotated): RMSNorm, W_q, RoPE at
+    `pos`, counter-causal attention (Eq. (2) under the Sec. 3.1 mask), W_o + residual,
+    RMSNorm, SwiGLU MLP + residual."""
+    R = len(rows)
+    a = rmsnorm(h, W["attn_norm"], eps)
+    q = (a @ f64(W["wq"]).T).reshape(R, n_heads_q, head_dim)
+    q = rope(q, pos, theta)
+    y = np.zeros((R, n_heads_q * head_dim))
+    for b in np.unique(seq):
+        lo, hi = int(cu[b]), int(cu[b + 1])
+        sel = np.nonzero(seq == b)[0]
+        n = hi - lo
+        qfull = np.zeros((n, n_heads_q, head_dim))
+        qfull[rows[sel] - lo] = q[sel]
+        o = attention_cc(qfull, K[:, lo:hi], V[:, lo:hi], diag, scale, rows[sel] - lo)
+        y[sel] = o.reshape(len(sel), -1)
+    h = h + y @ f64(W["wo"]).T
+    bn = rmsnorm(h, W["mlp_norm"], eps)
+    act = silu(bn @ f64(W["w_gate"]).T) * (bn @ f64(W["w_up"]).T)
+    return h + act @ f64(W["w_down"]).T
+
+
+def _rows_pos(cu_seqlens, rows, pos_ids):
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    N = int(cu[-1])
+    rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
+    seq = _rows_by_seq(cu, rows)
+    if pos_ids is None:
+        pos = rows - cu[seq]
+    else:
+        pos = np.asarray(pos_ids, dtype=np.int64)[rows]
+    return cu, rows, seq, pos
+
+
 def full_scores(ids, kv_layer: Callable, layer_weights: Callable, embed, final_norm_w,
                 w_lm, cu_seqlens, n_layers, n_heads_q, head_dim, theta, eps,
                 diag="strict", scale=None, pos_ids=None, n_frozen=0,
@@ -219,36 +255,30 @@ def full_scores(ids, kv_layer: Callable, layer_weights: Callable, embed, final_n
 
     kv_layer(l) -> (K_l, V_l) as [Hkv][N][d] (already rotated, as stored);
     layer_weights(l) -> dict(attn_norm, wq, wo, mlp_norm, w_gate, w_up, w_down)."""
-    cu = np.asarray(cu_seqlens, dtype=np.int64)
-    N = int(cu[-1])
-    rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
+    cu, rows, seq, pos = _rows_pos(cu_seqlens, rows, pos_ids)
     ids = np.asarray(ids, dtype=np.int64)
-    seq = _rows_by_seq(cu, rows)
-    if pos_ids is None:
-        pos = rows - cu[seq]
-    else:
-        pos = np.asarray(pos_ids, dtype=np.int64)[rows]
-    R = len(rows)
     h = f64(embed[ids[rows]])                                        # [R][D]
     for l in range(n_layers):
-        W = layer_weights(l)
         K, V = kv_layer(l)
-        a = rmsnorm(h, W["attn_norm"], eps)
-        q = (a @ f64(W["wq"]).T).reshape(R, n_heads_q, head_dim)
-        q = rope(q, pos, theta)
-        y = np.zeros((R, n_heads_q * head_dim))
-        for b in np.unique(seq):
-            lo, hi = int(cu[b]), int(cu[b + 1])
-            sel = np.nonzero(seq == b)[0]
-            n = hi - lo
-            qfull = np.zeros((n, n_heads_q, head_dim))
-            qfull[rows[sel] - lo] = q[sel]
-            o = attention_cc(qfull, K[:, lo:hi], V[:, lo:hi], diag, scale, rows[sel] - lo)
-            y[sel] = o.reshape(len(sel), -1)
-        h = h + y @ f64(W["wo"]).T
-        bn = rmsnorm(h, W["mlp_norm"], eps)
-        act = silu(bn @ f64(W["w_gate"]).T) * (bn @ f64(W["w_up"]).T)
-        h = h + act @ f64(W["w_down"]).T
+        h = _layer(h, layer_weights(l), K, V, rows, seq, pos, cu, n_heads_q, head_dim, theta,
+                   eps, diag, scale)
+    u = rmsnorm(h, final_norm_w, eps)
+    s, _, _ = surprise(u, w_lm, ids[rows])
+    s[edge_rows(cu, n_frozen)[rows]] = np.inf
+    return s
+
+
+def last_layer_h_scores(h_last, ids, K, V, W, final_norm_w, w_lm, cu_seqlens, n_heads_q,
+                        head_dim, theta, eps, diag="strict", scale=None, pos_ids=None,
+                        n_frozen=0, rows=None) -> np.ndarray:
+    """The fast single-layer approximation in its exact form (Sec. 3.1): the stored
+    activations H entering the last layer ([N][D]) go through that layer with fresh
+    queries (RoPE at the original positions) against the layer's stored K, V, then the
+    final RMSNorm and the LM head; scores as in Eq. (5) read as surprisal."""
+    cu, rows, seq, pos = _rows_pos(cu_seqlens, rows, pos_ids)
+    ids = np.asarray(ids, dtype=np.int64)
+    h = _layer(f64(np.asarray(h_last)[rows]), W, K, V, rows, seq, pos, cu, n_heads_q, head_dim,
+               theta, eps, diag, scale)
     u = rmsnorm(h, final_norm_w, eps)
     s, _, _ = surprise(u, w_lm, ids[rows])
     s[edge_rows(cu, n_frozen)[rows]] = np.inf

@@ -314,3 +314,88 @@ def test_full_pass_zero_query_weights_reduce_to_suffix_means():
     want = scipy.special.logsumexp(z, axis=1) - z[np.arange(n), t["ids"]]
     got = _oracle_full(t, 5e5, 1e-5)
     np.testing.assert_allclose(got[:-1], want[:-1], rtol=1e-12)
+
+
+# ---------------------------------------------------------------- exact fast variant
+
+def _torch_last_h(t, H, pos, theta, eps):
+    """One layer from H composed from torch library routines (as _torch_full), queries
+    rotated at the given original positions, then the final norm and log_softmax."""
+    F_ = torch.nn.functional
+    n, hq, hkv, d = t["n"], t["hq"], t["hkv"], t["d"]
+    g = hq // hkv
+    T = lambda a: torch.as_tensor(np.asarray(a, dtype=np.float64))
+    W = {k: T(v) for k, v in t["W"][-1].items()}
+    K, Vv = (T(x) for x in t["KV"][-1])
+    h = T(H)
+    inv = theta ** (-2.0 * torch.arange(d // 2, dtype=torch.float64) / d)
+    rot = torch.polar(torch.ones(n, d // 2, dtype=torch.float64),
+                      T(pos)[:, None] * inv[None])
+    allow = torch.triu(torch.ones(n, n, dtype=torch.bool), diagonal=1)
+    a = F_.rms_norm(h, (h.shape[-1],), W["attn_norm"], eps)
+    q = (a @ W["wq"].T).reshape(n, hq, d)
+    qc = torch.complex(q[..., : d // 2], q[..., d // 2:]) * rot[:, None, :]
+    q = torch.cat([qc.real, qc.imag], dim=-1)
+    o = F_.scaled_dot_product_attention(q.permute(1, 0, 2), K.repeat_interleave(g, 0),
+                                        Vv.repeat_interleave(g, 0), attn_mask=allow)
+    o = torch.nan_to_num(o.permute(1, 0, 2), nan=0.0)
+    h = h + o.reshape(n, -1) @ W["wo"].T
+    b = F_.rms_norm(h, (h.shape[-1],), W["mlp_norm"], eps)
+    h = h + (F_.silu(b @ W["w_gate"].T) * (b @ W["w_up"].T)) @ W["w_down"].T
+    u = F_.rms_norm(h, (h.shape[-1],), T(t["fn"]), eps)
+    logp = torch.log_softmax(u @ T(t["wl"]).T, dim=-1)
+    s = -logp[torch.arange(n), torch.as_tensor(t["ids"])].numpy()
+    s[-1] = np.inf
+    return s
+
+
+def _oracle_last_h(t, H, theta, eps, pos_ids=None, rows=None):
+    K, V = t["KV"][-1]
+    return O.last_layer_h_scores(H, t["ids"], K, V, t["W"][-1], t["fn"], t["wl"], [0, t["n"]],
+                                 t["hq"], t["d"], theta, eps, pos_ids=pos_ids, rows=rows)
+
+
+def test_last_layer_h_vs_library_composition():
+    """Stored activations of an arbitrary scale and original positions that are not
+    0..n-1 (as after earlier refreshes)."""
+    t = _tiny_full(seed=11, L=2)
+    r = np.random.default_rng(5)
+    H = 3.0 * r.standard_normal((t["n"], t["W"][0]["wq"].shape[1]))
+    pos = np.sort(r.choice(200, t["n"], replace=False))
+    theta, eps = 5e5, 1e-5
+    got = _oracle_last_h(t, H, theta, eps, pos_ids=pos)
+    np.testing.assert_allclose(got, _torch_last_h(t, H, pos, theta, eps), rtol=1e-10, atol=1e-10)
+    rows = [1, 5, 8]
+    np.testing.assert_allclose(_oracle_last_h(t, H, theta, eps, pos_ids=pos, rows=rows), got[rows],
+                               rtol=1e-13)
+
+
+def test_last_layer_h_with_embeddings_is_one_layer_full_pass():
+    t = _tiny_full(seed=12, L=1)
+    H = t["emb"][t["ids"]]
+    np.testing.assert_allclose(_oracle_last_h(t, H, 1e4, 1e-5), _oracle_full(t, 1e4, 1e-5),
+                               rtol=1e-13)
+
+
+def test_last_layer_h_zero_query_weights_closed_form():
+    """W_q = 0 gives uniform attention (suffix means of V); with W_down = 0 the final
+    hidden state is H + W_o (suffix means), a closed form."""
+    t = _tiny_full(seed=13, L=1)
+    t["W"][0]["wq"] = np.zeros_like(t["W"][0]["wq"])
+    t["W"][0]["w_down"] = np.zeros_like(t["W"][0]["w_down"])
+    r = np.random.default_rng(3)
+    n, hq, hkv, d = t["n"], t["hq"], t["hkv"], t["d"]
+    H = r.standard_normal((n, t["W"][0]["wq"].shape[1]))
+    V0 = t["KV"][0][1]
+    cs = np.cumsum(V0[:, ::-1], axis=1)[:, ::-1]
+    y = np.zeros((n, hq, d))
+    for i in range(n - 1):
+        for h in range(hq):
+            y[i, h] = cs[h // (hq // hkv), i + 1] / (n - 1 - i)
+    hfin = H + y.reshape(n, -1) @ t["W"][0]["wo"].T
+    u = hfin / np.sqrt((hfin ** 2).mean(-1, keepdims=True) + 1e-5) * t["fn"]
+    z = u @ t["wl"].T
+    want = scipy.special.logsumexp(z, axis=1) - z[np.arange(n), t["ids"]]
+    got = _oracle_last_h(t, H, 5e5, 1e-5)
+    np.testing.assert_allclose(got[:-1], want[:-1], rtol=1e-12)
+    assert got[-1] == np.inf
