@@ -163,6 +163,11 @@ def bench_generic(args, cfg, dev) -> dict:
     ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, per_head)), dtype=torch.uint8, device=dev)
     inp = w.inputs()
     stream = torch.cuda.current_stream()
+    h_rows = w.h_last if cfg.mode == "last_layer_h" else None
+    ws_rows = None
+    if h_rows is not None:
+        ws_rows = torch.empty(max(1, cc.cc_compact_rows_workspace(p, cfg.hidden * 2, per_head)),
+                              dtype=torch.uint8, device=dev)
 
     def step(ev=None):
         def mark(i):
@@ -174,6 +179,8 @@ def bench_generic(args, cfg, dev) -> dict:
         cc.cc_select_keep(scores, starts, lens, ks, keep, ws_sel)
         mark(2)
         cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp)
+        if h_rows is not None:        # the stored activations travel with their entries
+            cc.cc_compact_rows(p, h_rows, keep, ks, per_head, workspace=ws_rows)
         mark(3)
 
     for _ in range(args.warmup):
@@ -189,15 +196,19 @@ def bench_generic(args, cfg, dev) -> dict:
     part = {n: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, n in enumerate(names)}
     kept_rows = sum(ks) if per_head else sum(ks) * hkv            # (token, head) rows per layer
     moved = 2 * (2 * L * kept_rows * d * 2)                       # K and V, read + write
+    if cfg.mode == "last_layer_h":
+        moved += 2 * sum(cfg.keep) * cfg.hidden * 2                 # H rows, read + write
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     cmp_flushed = flushed_ms(lambda: cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp),
                              5, flush)
     hq, D, V = cfg.n_heads_q, cfg.hidden, cfg.vocab
     att_flop = 2.0 * d * hq * sum(n * (n - 1) for n in cfg.seq_lens)
     lm_flop = 2.0 * N * D * V
+    per_layer = 2.0 * N * D * (hq * d) * 2 + 2.0 * N * D * cfg.ffn * 3   # W_q, W_o, MLP
     if cfg.mode == "full":
-        per_layer = 2.0 * N * D * (hq * d) * 2 + 2.0 * N * D * cfg.ffn * 3
         score_flop = cfg.n_layers * (per_layer + att_flop) + lm_flop
+    elif cfg.mode == "last_layer_h":
+        score_flop = per_layer + att_flop + lm_flop
     else:
         score_flop = att_flop + 2.0 * N * D * hq * d + lm_flop
     return {

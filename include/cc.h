@@ -63,8 +63,17 @@ typedef enum cc_diag { CC_DIAG_STRICT = 0, CC_DIAG_INCLUSIVE = 1 } cc_diag;
 /* LAST_LAYER: the fast single-layer approximation (Sec. 3.1): queries are given,
  * attention runs on the cache's last layer, then W_o and the LM head.
  * FULL: every layer runs with fresh queries from the token embeddings against the
- * stored keys/values of that layer (Sec. 3.1, full counter-causal pass). */
-typedef enum cc_mode { CC_MODE_LAST_LAYER = 0, CC_MODE_FULL = 1 } cc_mode;
+ * stored keys/values of that layer (Sec. 3.1, full counter-causal pass).
+ * LAST_LAYER_H: the fast approximation in its exact form (Sec. 3.1, fast single-layer
+ * approximation): from the stored activations H entering the last layer, RMSNorm,
+ * W_q and RoPE at the original positions, attention on the cache's last layer, the
+ * layer's output processing (W_o + residual, RMSNorm, SwiGLU MLP + residual), the
+ * final RMSNorm and the LM head. */
+typedef enum cc_mode {
+  CC_MODE_LAST_LAYER = 0,
+  CC_MODE_FULL = 1,
+  CC_MODE_LAST_LAYER_H = 2
+} cc_mode;
 
 typedef enum cc_kv_layout { CC_KV_CONTIGUOUS = 0, CC_KV_PAGED = 1 } cc_kv_layout;
 
@@ -108,15 +117,15 @@ typedef struct cc_problem {
   int32_t hidden;              /* D: model width, rows of W_o */
   int32_t vocab;               /* V: rows of the LM head */
   int32_t n_layers;            /* FULL only: transformer layers (<= kv.n_layers) */
-  int32_t ffn;                 /* FULL only: SwiGLU width */
+  int32_t ffn;                 /* FULL, LAST_LAYER_H: SwiGLU width */
   float softmax_scale;         /* 0 selects 1/sqrt(head_dim) (Eq. (2)) */
-  float rope_theta;            /* FULL only: rotary base */
-  float rms_eps;               /* FULL only: RMSNorm epsilon */
+  float rope_theta;            /* FULL, LAST_LAYER_H: rotary base */
+  float rms_eps;               /* FULL, LAST_LAYER_H: RMSNorm epsilon */
   int32_t n_frozen;            /* first n_frozen entries of each sequence are sink
                                   slots that are never evicted (score +inf) */
 } cc_problem;
 
-/* Weights of one transformer layer (FULL mode), device pointers in `dtype`. */
+/* Weights of one transformer layer (FULL, LAST_LAYER_H), device pointers in `dtype`. */
 typedef struct cc_layer_weights {
   const void* attn_norm;       /* [D] RMSNorm gain before attention */
   const void* wq;              /* [Hq*d][D] query projection */
@@ -132,12 +141,16 @@ typedef struct cc_inputs {
   cc_kv kv;                    /* LAST_LAYER scores layer kv.n_layers-1; FULL uses
                                   layers 0..n_layers-1 (keys already rotated) */
   const int32_t* token_ids;    /* [N] cached token ids X */
-  const int32_t* pos_ids;      /* FULL: [N] original positions, NULL -> 0..n_b-1 */
+  const int32_t* pos_ids;      /* FULL, LAST_LAYER_H: [N] original positions,
+                                  NULL -> 0..n_b-1 */
   const void* w_o;             /* LAST_LAYER: [D][Hq*d] */
   const void* w_lm;            /* [V][D] LM head */
   const void* embed;           /* FULL: [V][D] token embeddings */
-  const cc_layer_weights* layers_h; /* FULL: host array [n_layers] */
-  const void* final_norm;      /* FULL: [D] final RMSNorm gain */
+  const cc_layer_weights* layers_h; /* FULL: host array [n_layers]; LAST_LAYER_H:
+                                  host array [1], the last layer's weights */
+  const void* final_norm;      /* FULL, LAST_LAYER_H: [D] final RMSNorm gain */
+  const void* h_last;          /* LAST_LAYER_H: [N][D] stored activations entering
+                                  the last layer (dtype), token-major like ids */
 } cc_inputs;
 
 /* Human-readable name of a status code (static string). */
@@ -223,6 +236,23 @@ cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* kee
                         const int32_t* k_h, int32_t per_head, int32_t* token_ids,
                         int32_t* pos_ids, const cc_kv* out, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/* Workspace for cc_compact_rows. */
+cc_status cc_compact_rows_workspace(const cc_problem* p, int32_t row_bytes, int32_t per_head,
+                                    size_t* bytes);
+
+/* Compaction of a token-major per-entry array that travels with the cache, such as the
+ * stored activations H of the exact fast variant (Sec. 3.1: H is recorded per cache
+ * entry, so the memory refresh of Sec. 3.2 keeps the same rows):
+ *   rows[cu[b] + j] = rows[cu[b] + keep_b[j]] for j < k_b,
+ * with the same keep lists as cc_compact_kv (per_head = 1: the first list of each
+ * sequence is used).  rows: device [N][row_bytes] (row_bytes a multiple of 16, rows
+ * 16-byte aligned); out_rows NULL compacts in place, else writes out_rows (same shape,
+ * no overlap with rows).  A bit copy. */
+cc_status cc_compact_rows(const cc_problem* p, void* rows, int32_t row_bytes,
+                          const int32_t* keep_idx, const int32_t* k_h, int32_t per_head,
+                          void* out_rows, void* workspace, size_t workspace_bytes,
+                          void* stream);
 
 #ifdef __cplusplus
 }

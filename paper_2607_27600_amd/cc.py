@@ -21,13 +21,14 @@ LIB_PATH = os.path.join(_HERE, "libcc.so")
 CC_OK, CC_ERR_ARG, CC_ERR_SHAPE, CC_ERR_DTYPE, CC_ERR_WORKSPACE, CC_ERR_UNSUPPORTED, CC_ERR_HIP = range(7)
 CC_F32, CC_BF16 = 0, 1
 CC_DIAG_STRICT, CC_DIAG_INCLUSIVE = 0, 1
-CC_MODE_LAST_LAYER, CC_MODE_FULL = 0, 1
+CC_MODE_LAST_LAYER, CC_MODE_FULL, CC_MODE_LAST_LAYER_H = 0, 1, 2
 CC_KV_CONTIGUOUS, CC_KV_PAGED = 0, 1
 
 EXPORTED = [
     "cc_status_str", "cc_version", "cc_score_workspace", "cc_score", "cc_attention_workspace",
     "cc_attention_cc", "cc_lmhead_workspace", "cc_lmhead_score", "cc_linear",
     "cc_select_workspace", "cc_select_keep", "cc_compact_workspace", "cc_compact_kv",
+    "cc_compact_rows_workspace", "cc_compact_rows",
 ]
 
 _c_void_p = ctypes.c_void_p
@@ -60,7 +61,8 @@ class c_layer_weights(ctypes.Structure):
 class c_inputs(ctypes.Structure):
     _fields_ = [("q", _c_void_p), ("kv", c_kv), ("token_ids", _c_void_p), ("pos_ids", _c_void_p),
                 ("w_o", _c_void_p), ("w_lm", _c_void_p), ("embed", _c_void_p),
-                ("layers_h", ctypes.POINTER(c_layer_weights)), ("final_norm", _c_void_p)]
+                ("layers_h", ctypes.POINTER(c_layer_weights)), ("final_norm", _c_void_p),
+                ("h_last", _c_void_p)]
 
 
 def _load():
@@ -89,6 +91,9 @@ def _load():
         "cc_compact_workspace": (st, [P(c_problem), _i32, _i32, sz]),
         "cc_compact_kv": (st, [P(c_problem), P(c_kv), _c_void_p, P(_i32), _i32, _c_void_p,
                                _c_void_p, P(c_kv), _c_void_p, ctypes.c_size_t, _c_void_p]),
+        "cc_compact_rows_workspace": (st, [P(c_problem), _i32, _i32, sz]),
+        "cc_compact_rows": (st, [P(c_problem), _c_void_p, _i32, _c_void_p, P(_i32), _i32,
+                                 _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -156,7 +161,8 @@ def problem(*, dtype: str, cu_seqlens: Sequence[int], n_heads_q: int, n_heads_kv
     cu_d = cu_h.to(device)
     s = c_problem()
     s.dtype = {"f32": CC_F32, "bf16": CC_BF16}[dtype]
-    s.mode = {"last_layer": CC_MODE_LAST_LAYER, "full": CC_MODE_FULL}[mode]
+    s.mode = {"last_layer": CC_MODE_LAST_LAYER, "full": CC_MODE_FULL,
+              "last_layer_h": CC_MODE_LAST_LAYER_H}[mode]
     s.diag = {"strict": CC_DIAG_STRICT, "inclusive": CC_DIAG_INCLUSIVE}[diag]
     s.n_seqs = len(cu_h) - 1
     s.cu_seqlens_h = ctypes.cast(cu_h.data_ptr(), ctypes.POINTER(_i32))
@@ -210,7 +216,8 @@ class Inputs:
 def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[torch.Tensor] = None,
            w_o: Optional[torch.Tensor] = None, pos_ids: Optional[torch.Tensor] = None,
            embed: Optional[torch.Tensor] = None, layers: Optional[list] = None,
-           final_norm: Optional[torch.Tensor] = None) -> Inputs:
+           final_norm: Optional[torch.Tensor] = None,
+           h_last: Optional[torch.Tensor] = None) -> Inputs:
     s = c_inputs()
     s.q = q.data_ptr() if q is not None else None
     s.kv = kv.struct
@@ -219,7 +226,8 @@ def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[t
     s.w_o = w_o.data_ptr() if w_o is not None else None
     s.w_lm = w_lm.data_ptr()
     s.embed = embed.data_ptr() if embed is not None else None
-    keep = [kv, token_ids, w_lm, q, w_o, pos_ids, embed, final_norm]
+    s.h_last = h_last.data_ptr() if h_last is not None else None
+    keep = [kv, token_ids, w_lm, q, w_o, pos_ids, embed, final_norm, h_last]
     if layers:
         arr = (c_layer_weights * len(layers))()
         for i, L in enumerate(layers):
@@ -324,3 +332,21 @@ def cc_compact_kv(p: Problem, kv: KV, keep_idx: torch.Tensor, k: Sequence[int], 
                               ctypes.byref(out.struct) if out is not None else None,
                               _ptr(workspace), workspace.numel(), _stream(stream)),
            "cc_compact_kv")
+
+
+def cc_compact_rows_workspace(p: Problem, row_bytes: int, per_head: int) -> int:
+    return _query(_lib.cc_compact_rows_workspace, ctypes.byref(p.struct), row_bytes, per_head)
+
+
+def cc_compact_rows(p: Problem, rows: torch.Tensor, keep_idx: torch.Tensor, k: Sequence[int],
+                    per_head: int, out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    """rows: [N][...] token-major; every entry row is compacted with its sequence's keep
+    list (in place unless `out` is given)."""
+    row_bytes = rows[0].numel() * rows.element_size() if rows.shape[0] else 16
+    kk = (_i32 * len(k))(*[int(x) for x in k])
+    if workspace is None:
+        workspace = _workspace(cc_compact_rows_workspace(p, row_bytes, per_head), p.device)
+    _check(_lib.cc_compact_rows(ctypes.byref(p.struct), _ptr(rows), row_bytes, _ptr(keep_idx), kk,
+                                per_head, _ptr(out), _ptr(workspace), workspace.numel(),
+                                _stream(stream)), "cc_compact_rows")

@@ -33,7 +33,9 @@ bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 cc_status check_problem(const cc_problem* p) {
   if (!p) return CC_ERR_ARG;
   if (p->dtype != CC_F32 && p->dtype != CC_BF16) return CC_ERR_DTYPE;
-  if (p->mode != CC_MODE_LAST_LAYER && p->mode != CC_MODE_FULL) return CC_ERR_ARG;
+  if (p->mode != CC_MODE_LAST_LAYER && p->mode != CC_MODE_FULL &&
+      p->mode != CC_MODE_LAST_LAYER_H)
+    return CC_ERR_ARG;
   if (p->diag != CC_DIAG_STRICT && p->diag != CC_DIAG_INCLUSIVE) return CC_ERR_ARG;
   if (p->n_seqs < 1 || !p->cu_seqlens_h || !p->cu_seqlens_d) return CC_ERR_ARG;
   if (p->cu_seqlens_h[0] != 0) return CC_ERR_SHAPE;
@@ -50,8 +52,8 @@ cc_status check_problem(const cc_problem* p) {
   } else {
     if (p->head_dim != 64 && p->head_dim != 128) return CC_ERR_UNSUPPORTED;
   }
-  if (p->mode == CC_MODE_FULL) {
-    if (p->n_layers < 1 || p->ffn < 1) return CC_ERR_SHAPE;
+  if (p->mode == CC_MODE_FULL || p->mode == CC_MODE_LAST_LAYER_H) {
+    if ((p->mode == CC_MODE_FULL && p->n_layers < 1) || p->ffn < 1) return CC_ERR_SHAPE;
     if (p->dtype != CC_BF16) return CC_ERR_UNSUPPORTED;
     if (p->ffn % 64 != 0) return CC_ERR_UNSUPPORTED;
     if (!(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return CC_ERR_ARG;
@@ -313,6 +315,50 @@ cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, vo
   return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
 }
 
+// The exact fast variant (Sec. 3.1, fast single-layer approximation): one layer of the
+// full pass, entered with the stored activations H instead of the embedding stack, on
+// the cache's last layer.
+cc_status score_last_h(const cc_problem* p, const cc_inputs* in, float* scores, void* ws,
+                       size_t ws_bytes, void* stream) {
+  CC_TRY(check_kv(p, &in->kv, 1));
+  const int N = n_tokens(p);
+  if (N > 0 && (!in->h_last || !in->layers_h || !in->final_norm || !in->w_lm ||
+                !in->token_ids || !scores))
+    return CC_ERR_ARG;
+  if (N > 0) {
+    if (!aligned16(in->h_last) || !aligned16(in->w_lm) || !aligned16(in->final_norm))
+      return CC_ERR_ARG;
+    const cc_layer_weights& W = in->layers_h[0];
+    const void* ptrs[7] = {W.attn_norm, W.wq, W.wo, W.mlp_norm, W.w_gate, W.w_up, W.w_down};
+    for (const void* q : ptrs)
+      if (!q || !aligned16(q)) return CC_ERR_ARG;
+  }
+  const FullLayout L = full_layout(p);
+  CC_TRY(check_ws(ws, ws_bytes, L.total));
+  if (N == 0) return CC_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int D = p->hidden, F = p->ffn, HD = p->n_heads_q * p->head_dim;
+  float2* rot = reinterpret_cast<float2*>(at(ws, L.rot));
+  float* h = reinterpret_cast<float*>(at(ws, L.h));
+  void* a = at(ws, L.a);
+  void* q = at(ws, L.q);
+  void* o = at(ws, L.o);
+  void* act = at(ws, L.act);
+  const cc_layer_weights& W = in->layers_h[0];
+  CC_HIP(launch_rope_table(in->pos_ids, p->cu_seqlens_d, p->n_seqs, rot, N, p->head_dim,
+                           double(p->rope_theta), s));
+  CC_HIP(launch_embed(in->h_last, nullptr, h, N, D, s));   // widen H to the fp32 stream
+  CC_HIP(launch_rmsnorm(h, W.attn_norm, a, N, D, p->rms_eps, s));
+  CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, s));
+  CC_TRY(run_attention(p, q, &in->kv, in->kv.n_layers - 1, o, at(ws, L.attn), s));
+  CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, s));
+  CC_HIP(launch_rmsnorm(h, W.mlp_norm, a, N, D, p->rms_eps, s));
+  CC_HIP(launch_gate_up_swiglu(W.w_gate, W.w_up, a, act, N, D, F, s));
+  CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
+  CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
+  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -383,7 +429,7 @@ cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_
 cc_status cc_score_workspace(const cc_problem* p, size_t* bytes) {
   if (!bytes) return CC_ERR_ARG;
   CC_TRY(check_problem(p));
-  *bytes = p->mode == CC_MODE_FULL ? full_layout(p).total : score_layout(p).total;
+  *bytes = p->mode == CC_MODE_LAST_LAYER ? score_layout(p).total : full_layout(p).total;
   return CC_OK;
 }
 
@@ -392,6 +438,7 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   CC_TRY(check_problem(p));
   if (!in) return CC_ERR_ARG;
   if (p->mode == CC_MODE_FULL) return score_full(p, in, scores, ws, ws_bytes, stream);
+  if (p->mode == CC_MODE_LAST_LAYER_H) return score_last_h(p, in, scores, ws, ws_bytes, stream);
   CC_TRY(check_kv(p, &in->kv, 1));
   const int N = n_tokens(p);
   if (N > 0 && (!in->q || !in->w_o || !in->w_lm || !in->token_ids || !scores)) return CC_ERR_ARG;
@@ -502,6 +549,7 @@ cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* kee
       const int k = k_h[li];
       if (k < 0 || k > n) return CC_ERR_SHAPE;
       plan.lists[li].keep_off = off;
+      plan.lists[li].tok0 = 0;
       plan.lists[li].k = k;
       plan.lists[li].pad = 0;
       off += k;
@@ -538,6 +586,7 @@ cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* kee
   CC_HIP(hipMemcpyAsync(at(ws, plan.off_seq), plan.seq_list.data(),
                         plan.seq_list.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
   CompactLaunch c;
+  c.n_tensors = 2;
   const cc_kv* dst = out ? out : kv;
   c.src[0] = make_view(kv, kv->k, es);
   c.src[1] = make_view(kv, kv->v, es);
@@ -556,6 +605,101 @@ cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* kee
   c.cu_d = p->cu_seqlens_d;
   c.seq_list_d = reinterpret_cast<const int32_t*>(at(ws, plan.off_seq));
   c.n_seqs = p->n_seqs;
+  CC_HIP(launch_compact(c, s));
+  return CC_OK;
+}
+
+// Token-major per-entry rows (e.g. the stored activations H) follow the keep lists of
+// the cache.  The rows are cut into column slabs of up to 256 bytes; each (sequence, slab)
+// is one plane of the compaction kernels, addressed through a flat view whose planes
+// start at the sequence's first row.
+namespace {
+int rows_slab_bytes(int row_bytes) {
+  int slab = 256;
+  while (slab > 16 && row_bytes % slab != 0) slab >>= 1;
+  return slab;
+}
+size_t rows_ws_bytes(const cc_problem* p, int row_bytes) {
+  const size_t n_slabs = size_t(row_bytes / rows_slab_bytes(row_bytes));
+  return align_up(size_t(p->n_seqs) * sizeof(CompactList)) +
+         align_up(size_t(p->n_seqs) * n_slabs * sizeof(CompactPlane));
+}
+}  // namespace
+
+cc_status cc_compact_rows_workspace(const cc_problem* p, int32_t row_bytes, int32_t per_head,
+                                    size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  if (per_head != 0 && per_head != 1) return CC_ERR_ARG;
+  if (row_bytes < 16 || row_bytes % 16 != 0) return CC_ERR_UNSUPPORTED;
+  *bytes = rows_ws_bytes(p, row_bytes);
+  return CC_OK;
+}
+
+cc_status cc_compact_rows(const cc_problem* p, void* rows, int32_t row_bytes,
+                          const int32_t* keep_idx, const int32_t* k_h, int32_t per_head,
+                          void* out_rows, void* ws, size_t ws_bytes, void* stream) {
+  CC_TRY(check_problem(p));
+  if (per_head != 0 && per_head != 1) return CC_ERR_ARG;
+  if (row_bytes < 16 || row_bytes % 16 != 0) return CC_ERR_UNSUPPORTED;
+  if (!k_h) return CC_ERR_ARG;
+  const int hkv = p->n_heads_kv;
+  const int slab = rows_slab_bytes(row_bytes), n_slabs = row_bytes / slab;
+  std::vector<CompactList> lists(p->n_seqs);
+  std::vector<CompactPlane> planes;
+  int64_t off = 0;
+  int max_k = 0;
+  for (int b = 0; b < p->n_seqs; ++b) {
+    const int n = p->cu_seqlens_h[b + 1] - p->cu_seqlens_h[b];
+    for (int h = 0; h < (per_head ? hkv : 1); ++h) {
+      const int li = per_head ? b * hkv + h : b;
+      if (k_h[li] < 0 || k_h[li] > n) return CC_ERR_SHAPE;
+      if (h == 0) {   // the sequence's first list
+        lists[b].keep_off = off;
+        lists[b].tok0 = p->cu_seqlens_h[b];
+        lists[b].k = k_h[li];
+        lists[b].pad = 0;
+        max_k = std::max(max_k, k_h[li]);
+      }
+      off += k_h[li];
+    }
+  }
+  if (off > 0 && (!keep_idx || !rows)) return CC_ERR_ARG;
+  if ((rows && !aligned16(rows)) || (out_rows && !aligned16(out_rows))) return CC_ERR_ARG;
+  for (int b = 0; b < p->n_seqs; ++b)
+    if (lists[b].k > 0)
+      for (int h = 0; h < n_slabs; ++h) planes.push_back(CompactPlane{b, 0, h, b});
+  const size_t off_planes = align_up(size_t(p->n_seqs) * sizeof(CompactList));
+  CC_TRY(check_ws(ws, ws_bytes, rows_ws_bytes(p, row_bytes)));
+  if (planes.empty()) return CC_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  CC_HIP(hipMemcpyAsync(ws, lists.data(), lists.size() * sizeof(CompactList),
+                        hipMemcpyHostToDevice, s));
+  CC_HIP(hipMemcpyAsync(at(ws, off_planes), planes.data(), planes.size() * sizeof(CompactPlane),
+                        hipMemcpyHostToDevice, s));
+  auto view = [&](void* base) {
+    KvView v{};
+    v.base = base;
+    v.head_stride = slab;      // bytes: column slab h
+    v.tok_stride = row_bytes;  // bytes: one entry
+    return v;
+  };
+  CompactLaunch c;
+  c.n_tensors = 1;
+  c.src[0] = c.src[1] = view(rows);
+  c.dst[0] = c.dst[1] = view(out_rows ? out_rows : rows);
+  c.paged = false;
+  c.row_bytes = slab;
+  c.keep = keep_idx;
+  c.lists_d = static_cast<const CompactList*>(ws);
+  c.planes_d = reinterpret_cast<const CompactPlane*>(at(ws, off_planes));
+  c.n_planes = int(planes.size());
+  c.max_k = max_k;
+  c.in_place = out_rows == nullptr;
+  c.ids[0] = c.ids[1] = nullptr;
+  c.cu_d = p->cu_seqlens_d;
+  c.seq_list_d = nullptr;
+  c.n_seqs = 0;
   CC_HIP(launch_compact(c, s));
   return CC_OK;
 }

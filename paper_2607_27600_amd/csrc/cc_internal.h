@@ -126,11 +126,13 @@ struct CompactPlane {
 };
 struct CompactList {
   int64_t keep_off;  // offset of the list in keep_idx
+  int64_t tok0;      // first row of the sequence in a flat token-major array (0 for caches)
   int32_t k;
   int32_t pad;
 };
 struct CompactLaunch {
   KvView src[2], dst[2];   // keys, values; strides in BYTES
+  int n_tensors;           // 2 (keys and values) or 1
   bool paged;
   int row_bytes;           // head_dim * element size
   const int32_t* keep;
@@ -157,7 +159,7 @@ hipError_t launch_linear_residual(const void* x, const void* w, float* h, int M,
 // act[n][f] = silu(W_gate b[n])[f] * (W_up b[n])[f].
 hipError_t launch_gate_up_swiglu(const void* w_gate, const void* w_up, const void* b, void* act,
                                  int N, int D, int F, hipStream_t s);
-// h[n][:] = embed[ids[n]][:] (bf16 -> fp32).
+// h[n][:] = embed[ids[n]][:] (bf16 -> fp32); ids == null widens row n of `embed`.
 hipError_t launch_embed(const void* embed, const int32_t* ids, float* h, int N, int D,
                         hipStream_t s);
 // y[n][:] = bf16(h[n][:] / sqrt(mean(h[n]^2) + eps) * gamma).

@@ -119,7 +119,7 @@ __global__ __launch_bounds__(CNT) void compact_in_place_kernel(CompactArgs a) {
   const int k = L.k;
   if (k <= 0) return;
   const KvView& v = a.src[tensor];   // source and destination views are the same
-  char* base = reinterpret_cast<char*>(const_cast<void*>(v.base));
+  char* base = reinterpret_cast<char*>(const_cast<void*>(v.base)) + L.tok0 * v.tok_stride;
   const int tpr = a.row16;
   const int sub = threadIdx.x % tpr;
   const int r0 = threadIdx.x / tpr;
@@ -186,8 +186,8 @@ __global__ __launch_bounds__(CNT) void compact_kernel(CompactArgs a) {
   const int k = L.k;
   const KvView& sv = a.src[tensor];
   const KvView& dv = a.dst[tensor];
-  const char* sb = reinterpret_cast<const char*>(sv.base);
-  char* db = reinterpret_cast<char*>(const_cast<void*>(dv.base));
+  const char* sb = reinterpret_cast<const char*>(sv.base) + L.tok0 * sv.tok_stride;
+  char* db = reinterpret_cast<char*>(const_cast<void*>(dv.base)) + L.tok0 * dv.tok_stride;
   const int tpr = a.row16;
   const int sub = threadIdx.x % tpr;
   const int r0 = threadIdx.x / tpr;
@@ -258,14 +258,14 @@ hipError_t launch_compact(const CompactLaunch& c, hipStream_t s) {
   a.rows_per_chunk = (CNT / a.row16) * CU;
   if (c.n_planes > 0) {
     if (c.in_place) {
-      dim3 grid(2 * c.n_planes);
+      dim3 grid(c.n_tensors * c.n_planes);
       if (c.paged)
         hipLaunchKernelGGL(compact_in_place_kernel<true>, grid, dim3(CNT), 0, s, a);
       else
         hipLaunchKernelGGL(compact_in_place_kernel<false>, grid, dim3(CNT), 0, s, a);
     } else {
       // chunks sized by the longest list; planes with shorter lists exit early
-      dim3 grid(2 * c.n_planes, (c.max_k + a.rows_per_chunk - 1) / a.rows_per_chunk);
+      dim3 grid(c.n_tensors * c.n_planes, (c.max_k + a.rows_per_chunk - 1) / a.rows_per_chunk);
       if (grid.y > 0) {
         if (c.paged)
           hipLaunchKernelGGL(compact_kernel<true>, grid, dim3(CNT), 0, s, a);

@@ -13,7 +13,7 @@ __global__ __launch_bounds__(RNT) void embed_kernel(const u16* __restrict__ embe
                                                     const int32_t* __restrict__ ids,
                                                     float* __restrict__ h, int D) {
   const int n = blockIdx.x;
-  const u16* row = embed + int64_t(ids[n]) * D;
+  const u16* row = embed + int64_t(ids ? ids[n] : n) * D;   // no ids: widen row n
   float* out = h + int64_t(n) * D;
   for (int i = threadIdx.x * 4; i < D; i += RNT * 4) {
     const uint2 v = *reinterpret_cast<const uint2*>(row + i);

@@ -56,6 +56,17 @@ class Workload:
             self.w_o = to_device(wo, device)
             if keep_host:
                 self.host.update(q=q, w_o=wo)
+        elif cfg.mode == "last_layer_h":
+            self.q = None
+            self.w_o = None
+            hl = C.draw_h_last(cfg)
+            self.h_last = to_device(hl, device)
+            W = C.draw_layer_weights(cfg, cfg.n_layers - 1)
+            self.layers = [{k: to_device(v, device) for k, v in W.items()}]
+            fn = C.final_norm(cfg)
+            self.final_norm = to_device(fn, device)
+            if keep_host:
+                self.host.update(h_last=hl, layer=W, final_norm=fn)
         else:
             self.q = None
             self.w_o = None
@@ -134,6 +145,9 @@ class Workload:
                                        head_stride=cap * d, tok_stride=d)
 
     def inputs(self) -> cc.Inputs:
+        if self.cfg.mode == "last_layer_h":
+            return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=self.w_lm, layers=self.layers,
+                             final_norm=self.final_norm, h_last=self.h_last)
         if self.cfg.mode == "full":
             return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=self.w_lm, embed=self.embed,
                              layers=self.layers, final_norm=self.final_norm)

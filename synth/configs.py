@@ -18,7 +18,7 @@ import numpy as np
 from . import gen
 
 # tensor ids (per-layer tensors add the layer index)
-T_Q, T_WO, T_WLM, T_IDS, T_LENS, T_PAGES, T_EMBED = 1, 4, 5, 6, 7, 8, 9
+T_Q, T_WO, T_WLM, T_IDS, T_LENS, T_PAGES, T_EMBED, T_H = 1, 4, 5, 6, 7, 8, 9, 10
 T_K_LAYER, T_V_LAYER = 1000, 2000
 T_WQ, T_WO_L, T_WG, T_WU, T_WD = 3000, 4000, 5000, 6000, 7000
 
@@ -27,7 +27,7 @@ T_WQ, T_WO_L, T_WG, T_WU, T_WD = 3000, 4000, 5000, 6000, 7000
 class Config:
     name: str
     dtype: str                 # "f32" or "bf16"
-    mode: str                  # "last_layer" or "full"
+    mode: str                  # "last_layer", "full" or "last_layer_h"
     seq_lens: tuple            # cached tokens per sequence
     n_heads_q: int
     n_heads_kv: int
@@ -39,7 +39,7 @@ class Config:
     per_head_select: bool = False
     paged: bool = False
     page_size: int = 16
-    n_layers: int = 1          # FULL: transformer layers run
+    n_layers: int = 1          # FULL: transformer layers run; LAST_LAYER_H: model depth
     ffn: int = 0
     rope_theta: float = 5e5
     rms_eps: float = 1e-5
@@ -93,7 +93,13 @@ C5 = Config("C5", "bf16", "last_layer", _C5_LENS, 28, 4, 128, 3584, 152064, 28,
             description="ragged batch of 8, lengths U[2048,16384], Qwen2.5-7B shapes "
                         "(28q/4kv, hidden 3584, vocab 152064), paged cache P=16, keep 20%")
 
-CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5)}
+C2H = Config("C2H", "bf16", "last_layer_h", (4096,), 32, 8, 128, 4096, 128256, 32, (1024,),
+             n_layers=32, ffn=14336,
+             description="Llama-3-8B shapes, exact fast variant from the stored activations "
+                         "entering the last layer, bf16: n=4096, SwiGLU 14336, keep 25%, "
+                         "32-layer cache")
+
+CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5, C2H)}
 
 
 def shrink(cfg: Config, **kw) -> Config:
@@ -121,6 +127,12 @@ def widen(cfg: Config, a: np.ndarray) -> np.ndarray:
 def draw_q(cfg: Config) -> np.ndarray:
     """Queries [N][Hq][d], N(0,1)."""
     return _normal(cfg, T_Q, (cfg.n_tokens, cfg.n_heads_q, cfg.head_dim), 1.0)
+
+
+def draw_h_last(cfg: Config) -> np.ndarray:
+    """Stored activations entering the last layer [N][D], N(0,1) (RMSNorm makes the
+    layer insensitive to their overall scale)."""
+    return _normal(cfg, T_H, (cfg.n_tokens, cfg.hidden), 1.0)
 
 
 def draw_kv_layer(cfg: Config, layer: int, which: str) -> np.ndarray:
