@@ -8,7 +8,7 @@ import torch
 from oracle import cc_oracle as O
 from synth import configs as C
 from synth import gen
-from tests.gpu_util import assert_scores_close, dev, f64
+from tests.gpu_util import assert_scores_close, bf16_host, dev, f64
 
 pytestmark = pytest.mark.gpu
 
@@ -122,3 +122,48 @@ def test_score_c2_full_size_sampled():
     rows = C.sample_rows(C.C2, count=64)
     got, ref = _score_case(C.C2, rows=rows)
     print(assert_scores_close(got, ref, "bf16", "C2"))
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_empty_sequences_through_the_refresh(paged):
+    """Zero-length sequences inside a ragged batch: scores of the others are unaffected,
+    empty segments select nothing, and compaction leaves every other plane exact."""
+    from paper_2607_27600_amd import cc
+    cfg = C.shrink(C.C5, seq_lens=(5, 0, 130, 0, 1), hidden=512, vocab=3000, cache_layers=2,
+                   keep=(2, 0, 30, 0, 1), paged=paged)
+    got, ref = _score_case(cfg)
+    print(assert_scores_close(got, ref, "bf16", "empty-seqs"))
+    from paper_2607_27600_amd.workload import Workload
+    w = Workload(cfg, keep_host=True)
+    scores = torch.from_numpy(got.astype(np.float32)).cuda()
+    cu = cfg.cu_seqlens
+    ks = list(cfg.keep)
+    keep = torch.full((max(1, sum(ks)),), -7, dtype=torch.int32, device="cuda")
+    cc.cc_select_keep(scores, [int(x) for x in cu[:-1]], list(cfg.seq_lens), ks, keep)
+    torch.cuda.synchronize()
+    kk = keep.cpu().numpy()
+    lists, off = [], 0
+    for b, n in enumerate(cfg.seq_lens):
+        ref_l = O.select_keep(got[cu[b]:cu[b + 1]], ks[b])
+        np.testing.assert_array_equal(kk[off:off + ks[b]], ref_l)
+        lists.append(ref_l)
+        off += ks[b]
+    k_before = bf16_host(w.k_cache)
+    ids_before = w.ids.cpu().numpy()
+    cc.cc_compact_kv(w.problem, w.kv, keep, ks, 0, w.ids)
+    torch.cuda.synchronize()
+    k_after = bf16_host(w.k_cache)
+    bt = w.block_table.cpu().numpy() if paged else None
+    for b, lst in enumerate(lists):
+        for l in range(2):
+            for h in range(cfg.n_heads_kv):
+                for j, t in enumerate(lst):
+                    if paged:
+                        P = cfg.page_size
+                        src = k_before[l, bt[b, t // P], h, t % P]
+                        dst = k_after[l, bt[b, j // P], h, j % P]
+                    else:
+                        src, dst = k_before[b, l, h, t], k_after[b, l, h, j]
+                    np.testing.assert_array_equal(dst, src)
+        np.testing.assert_array_equal(w.ids.cpu().numpy()[cu[b]:cu[b] + len(lst)],
+                                      ids_before[cu[b] + lst])
