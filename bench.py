@@ -300,6 +300,53 @@ def bench_loop(args, dev) -> dict:
     }
 
 
+def fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len, ws_sel, ws_cmp,
+                      out_kv, stream, ms_two_step):
+    """Steps of the fast variant with W_o folded into the LM head (LAST_LAYER_FUSED)."""
+    import torch
+    N, Hq, d, V = cfg.n_tokens, cfg.n_heads_q, cfg.head_dim, cfg.vocab
+    dev = scores.device
+    pf = cc.problem(dtype="bf16", cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=Hq,
+                    n_heads_kv=cfg.n_heads_kv, head_dim=d, hidden=cfg.hidden, vocab=V,
+                    device=dev, mode="last_layer_fused")
+    m = torch.empty((V, Hq * d), dtype=torch.bfloat16, device=dev)
+    ws_fuse = torch.empty(cc.cc_fuse_wo_lmhead_workspace("bf16", cfg.hidden, Hq * d),
+                          dtype=torch.uint8, device=dev)
+    cc.cc_fuse_wo_lmhead("bf16", w.w_lm, w.w_o, out=m, workspace=ws_fuse)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    cc.cc_fuse_wo_lmhead("bf16", w.w_lm, w.w_o, out=m, workspace=ws_fuse)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    fuse_ms = ev[0].elapsed_time(ev[1])
+    del ws_fuse
+    inp = cc.inputs(kv=w.kv, token_ids=w.ids, w_lm=m, q=w.q)
+    ws = torch.empty(cc.cc_score_workspace(pf), dtype=torch.uint8, device=dev)
+    s_fused = torch.empty_like(scores)
+
+    def fstep():
+        cc.cc_score(pf, inp, s_fused, workspace=ws)
+        cc.cc_select_keep(s_fused, seg_start, seg_len, ks, keep, ws_sel)
+        cc.cc_compact_kv(pf, w.kv, keep, ks, int(cfg.per_head_select), out=out_kv, workspace=ws_cmp)
+
+    for _ in range(max(1, args.warmup)):
+        fstep()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fstep()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    fin = torch.isfinite(scores)
+    diff = float((s_fused[fin] - scores[fin]).abs().max().item()) if bool(fin.any()) else 0.0
+    del m, ws
+    return {"ms_per_step": ms, "tokens_per_s": N / (ms * 1e-3),
+            "speedup_vs_two_step": ms_two_step / ms, "fuse_weight_ms": fuse_ms,
+            "max_abs_score_diff_vs_two_step": diff,
+            "note": "W_lm W_o made once per model (fuse_weight_ms, outside the step); step = "
+                    "attention -> LM head on the product -> select -> compaction"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -401,6 +448,12 @@ def main():
             part_ms[n] += e[j].elapsed_time(e[j + 1]) / args.steps
     ms_step = elapsed * 1e3 / args.steps
 
+    # NEXT-4 alternative: W_o folded into the LM head (mode LAST_LAYER_FUSED).  The product
+    # weight is made once per model (timed apart, not part of a step); a fused step is
+    # attention -> LM head on the product -> select -> compaction.
+    fused = fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len, ws_sel,
+                              ws_cmp, out_kv, stream, ms_step)
+
     # in-place compaction (what a refresh does to the live cache), timed on its own after
     # the steps: every call moves the same bytes
     ev_ip = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -459,6 +512,7 @@ def main():
                              "gb_s_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9,
                              "frac_hbm_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "select_sweep": sweep,
+        "fused_wo_lmhead": fused,
         "breakdown_ms": part_ms,
         "wo_proj_tflops": wo_flop / (part_ms["wo_proj"] * 1e-3) / 1e12,
         "input_generation_s": t_gen,

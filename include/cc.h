@@ -68,11 +68,17 @@ typedef enum cc_diag { CC_DIAG_STRICT = 0, CC_DIAG_INCLUSIVE = 1 } cc_diag;
  * approximation): from the stored activations H entering the last layer, RMSNorm,
  * W_q and RoPE at the original positions, attention on the cache's last layer, the
  * layer's output processing (W_o + residual, RMSNorm, SwiGLU MLP + residual), the
- * final RMSNorm and the LM head. */
+ * final RMSNorm and the LM head.
+ * LAST_LAYER_FUSED: LAST_LAYER with W_o folded into the LM head.  With queries given,
+ * the output processing of the fast approximation (Sec. 3.1) is the bare projection
+ * W_o, so z = W_lm (W_o y) = (W_lm W_o) y: inputs.w_lm holds the product
+ * [V][Hq*head_dim] (from cc_fuse_wo_lmhead, once per model) and inputs.w_o is unused.
+ * The scores equal LAST_LAYER's up to rounding. */
 typedef enum cc_mode {
   CC_MODE_LAST_LAYER = 0,
   CC_MODE_FULL = 1,
-  CC_MODE_LAST_LAYER_H = 2
+  CC_MODE_LAST_LAYER_H = 2,
+  CC_MODE_LAST_LAYER_FUSED = 3
 } cc_mode;
 
 typedef enum cc_kv_layout { CC_KV_CONTIGUOUS = 0, CC_KV_PAGED = 1 } cc_kv_layout;
@@ -137,14 +143,16 @@ typedef struct cc_layer_weights {
 } cc_layer_weights;
 
 typedef struct cc_inputs {
-  const void* q;               /* LAST_LAYER: [N][Hq][d] queries (already rotated) */
+  const void* q;               /* LAST_LAYER(_FUSED): [N][Hq][d] queries (already
+                                  rotated) */
   cc_kv kv;                    /* LAST_LAYER scores layer kv.n_layers-1; FULL uses
                                   layers 0..n_layers-1 (keys already rotated) */
   const int32_t* token_ids;    /* [N] cached token ids X */
   const int32_t* pos_ids;      /* FULL, LAST_LAYER_H: [N] original positions,
                                   NULL -> 0..n_b-1 */
   const void* w_o;             /* LAST_LAYER: [D][Hq*d] */
-  const void* w_lm;            /* [V][D] LM head */
+  const void* w_lm;            /* [V][D] LM head; LAST_LAYER_FUSED: [V][Hq*d], the
+                                  product W_lm W_o */
   const void* embed;           /* FULL: [V][D] token embeddings */
   const cc_layer_weights* layers_h; /* FULL: host array [n_layers]; LAST_LAYER_H:
                                   host array [1], the last layer's weights */
@@ -194,6 +202,18 @@ cc_status cc_lmhead_workspace(const cc_problem* p, size_t* bytes);
 cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
                           const int32_t* token_ids, float* scores, float* lse,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace for cc_fuse_wo_lmhead: the transposed W_o. */
+cc_status cc_fuse_wo_lmhead_workspace(int32_t dtype, int32_t hidden, int32_t qdim,
+                                      size_t* bytes);
+
+/* The weight of mode LAST_LAYER_FUSED: out[v][c] = sum_d w_lm[v][d] w_o[d][c], with
+ * w_lm [V][hidden], w_o [hidden][qdim] (qdim = Hq*head_dim) and out [V][qdim], all in
+ * dtype (fp32 accumulation, one rounding to dtype).  A one-time weight preparation,
+ * not part of a refresh.  bf16 needs hidden % 64 == 0 and 16-byte aligned pointers. */
+cc_status cc_fuse_wo_lmhead(int32_t dtype, const void* w_lm, const void* w_o, void* out,
+                            int32_t vocab, int32_t hidden, int32_t qdim, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /* Dense projection y[m][n] = sum_k x[m][k] w[n][k] (x: [M][K], w: [N][K], y: [M][N],
  * all in dtype), the layer's output projection of the fast variant. */

@@ -151,9 +151,9 @@ def _rows_by_seq(cu, rows):
 # fast (last-layer) variant
 # ----------------------------------------------------------------------------------
 
-def last_layer_hidden(q, k, v, w_o, cu_seqlens, diag="strict", scale=None,
-                      rows=None) -> np.ndarray:
-    """u_i = W_o concat_h(o_{i,h}) for the requested global rows.
+def attention_rows(q, k, v, cu_seqlens, diag="strict", scale=None, rows=None) -> np.ndarray:
+    """y_i = concat_h(o_{i,h}), the counter-causal attention output of the requested
+    global rows, head-major.
 
     q: [N][Hq][d]; k, v: [Hkv][N][d] (sequences concatenated by cu_seqlens)."""
     cu = np.asarray(cu_seqlens, dtype=np.int64)
@@ -168,7 +168,13 @@ def last_layer_hidden(q, k, v, w_o, cu_seqlens, diag="strict", scale=None,
         local = rows[sel] - lo
         o = attention_cc(q[lo:hi], k[:, lo:hi], v[:, lo:hi], diag, scale, local)
         y[sel] = o.reshape(len(sel), hq * d)
-    return y @ f64(w_o).T
+    return y
+
+
+def last_layer_hidden(q, k, v, w_o, cu_seqlens, diag="strict", scale=None,
+                      rows=None) -> np.ndarray:
+    """u_i = W_o concat_h(o_{i,h}) for the requested global rows."""
+    return attention_rows(q, k, v, cu_seqlens, diag, scale, rows) @ f64(w_o).T
 
 
 def last_layer_scores(q, k, v, w_o, w_lm, ids, cu_seqlens, diag="strict", scale=None,
@@ -179,6 +185,25 @@ def last_layer_scores(q, k, v, w_o, w_lm, ids, cu_seqlens, diag="strict", scale=
     rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
     u = last_layer_hidden(q, k, v, w_o, cu, diag, scale, rows)
     s, _, _ = surprise(u, w_lm, np.asarray(ids)[rows])
+    s[edge_rows(cu, n_frozen)[rows]] = np.inf
+    return s
+
+
+def fused_lmhead_weight(w_lm, w_o) -> np.ndarray:
+    """M = W_lm W_o, [V][Hq*d].  With the queries given, the fast variant's output
+    processing is the bare projection W_o (Sec. 3.1), so z = W_lm (W_o y) = M y."""
+    return f64(w_lm) @ f64(w_o)
+
+
+def last_layer_fused_scores(q, k, v, w_fused, ids, cu_seqlens, diag="strict", scale=None,
+                            n_frozen=0, rows=None) -> np.ndarray:
+    """Surprise scores of the fast variant with the LM head applied to the attention rows
+    through a given product weight w_fused = W_lm W_o [V][Hq*d]."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    N = int(cu[-1])
+    rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
+    y = attention_rows(q, k, v, cu, diag, scale, rows)
+    s, _, _ = surprise(y, w_fused, np.asarray(ids)[rows])
     s[edge_rows(cu, n_frozen)[rows]] = np.inf
     return s
 

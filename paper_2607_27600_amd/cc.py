@@ -21,14 +21,15 @@ LIB_PATH = os.path.join(_HERE, "libcc.so")
 CC_OK, CC_ERR_ARG, CC_ERR_SHAPE, CC_ERR_DTYPE, CC_ERR_WORKSPACE, CC_ERR_UNSUPPORTED, CC_ERR_HIP = range(7)
 CC_F32, CC_BF16 = 0, 1
 CC_DIAG_STRICT, CC_DIAG_INCLUSIVE = 0, 1
-CC_MODE_LAST_LAYER, CC_MODE_FULL, CC_MODE_LAST_LAYER_H = 0, 1, 2
+CC_MODE_LAST_LAYER, CC_MODE_FULL, CC_MODE_LAST_LAYER_H, CC_MODE_LAST_LAYER_FUSED = 0, 1, 2, 3
 CC_KV_CONTIGUOUS, CC_KV_PAGED = 0, 1
 
 EXPORTED = [
     "cc_status_str", "cc_version", "cc_score_workspace", "cc_score", "cc_attention_workspace",
     "cc_attention_cc", "cc_lmhead_workspace", "cc_lmhead_score", "cc_linear",
     "cc_select_workspace", "cc_select_keep", "cc_compact_workspace", "cc_compact_kv",
-    "cc_compact_rows_workspace", "cc_compact_rows",
+    "cc_compact_rows_workspace", "cc_compact_rows", "cc_fuse_wo_lmhead_workspace",
+    "cc_fuse_wo_lmhead",
 ]
 
 _c_void_p = ctypes.c_void_p
@@ -85,6 +86,9 @@ def _load():
         "cc_lmhead_score": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                  _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p]),
         "cc_linear": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32, _c_void_p]),
+        "cc_fuse_wo_lmhead_workspace": (st, [_i32, _i32, _i32, sz]),
+        "cc_fuse_wo_lmhead": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32,
+                                   _c_void_p, ctypes.c_size_t, _c_void_p]),
         "cc_select_workspace": (st, [_i32, sz]),
         "cc_select_keep": (st, [_c_void_p, _i32, P(_i64), P(_i32), P(_i32), _c_void_p, _c_void_p,
                                 ctypes.c_size_t, _c_void_p]),
@@ -162,7 +166,8 @@ def problem(*, dtype: str, cu_seqlens: Sequence[int], n_heads_q: int, n_heads_kv
     s = c_problem()
     s.dtype = {"f32": CC_F32, "bf16": CC_BF16}[dtype]
     s.mode = {"last_layer": CC_MODE_LAST_LAYER, "full": CC_MODE_FULL,
-              "last_layer_h": CC_MODE_LAST_LAYER_H}[mode]
+              "last_layer_h": CC_MODE_LAST_LAYER_H,
+              "last_layer_fused": CC_MODE_LAST_LAYER_FUSED}[mode]
     s.diag = {"strict": CC_DIAG_STRICT, "inclusive": CC_DIAG_INCLUSIVE}[diag]
     s.n_seqs = len(cu_h) - 1
     s.cu_seqlens_h = ctypes.cast(cu_h.data_ptr(), ctypes.POINTER(_i32))
@@ -288,6 +293,30 @@ def cc_lmhead_score(p: Problem, u: torch.Tensor, w_lm: torch.Tensor, token_ids: 
                                 _ptr(scores), _ptr(lse), _ptr(workspace), workspace.numel(),
                                 _stream(stream)), "cc_lmhead_score")
     return scores
+
+
+def cc_fuse_wo_lmhead_workspace(dtype: str, hidden: int, qdim: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib.cc_fuse_wo_lmhead_workspace({"f32": CC_F32, "bf16": CC_BF16}[dtype], hidden, qdim,
+                                            ctypes.byref(n)), "cc_fuse_wo_lmhead_workspace")
+    return n.value
+
+
+def cc_fuse_wo_lmhead(dtype: str, w_lm: torch.Tensor, w_o: torch.Tensor,
+                      out: Optional[torch.Tensor] = None, workspace=None, stream=None):
+    """The LAST_LAYER_FUSED weight W_lm W_o [V][Hq*d] from w_lm [V][D] and w_o [D][Hq*d]."""
+    V, D = w_lm.shape
+    D2, Q = w_o.shape
+    if D2 != D:
+        raise ValueError(f"w_o has {D2} rows, w_lm has {D} columns")
+    if out is None:
+        out = torch.empty((V, Q), dtype=w_lm.dtype, device=w_lm.device)
+    if workspace is None:
+        workspace = _workspace(cc_fuse_wo_lmhead_workspace(dtype, D, Q), w_lm.device)
+    _check(_lib.cc_fuse_wo_lmhead({"f32": CC_F32, "bf16": CC_BF16}[dtype], _ptr(w_lm), _ptr(w_o),
+                                  _ptr(out), V, D, Q, _ptr(workspace), workspace.numel(),
+                                  _stream(stream)), "cc_fuse_wo_lmhead")
+    return out
 
 
 def cc_linear(dtype: str, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, stream=None):

@@ -34,7 +34,7 @@ cc_status check_problem(const cc_problem* p) {
   if (!p) return CC_ERR_ARG;
   if (p->dtype != CC_F32 && p->dtype != CC_BF16) return CC_ERR_DTYPE;
   if (p->mode != CC_MODE_LAST_LAYER && p->mode != CC_MODE_FULL &&
-      p->mode != CC_MODE_LAST_LAYER_H)
+      p->mode != CC_MODE_LAST_LAYER_H && p->mode != CC_MODE_LAST_LAYER_FUSED)
     return CC_ERR_ARG;
   if (p->diag != CC_DIAG_STRICT && p->diag != CC_DIAG_INCLUSIVE) return CC_ERR_ARG;
   if (p->n_seqs < 1 || !p->cu_seqlens_h || !p->cu_seqlens_d) return CC_ERR_ARG;
@@ -199,7 +199,7 @@ ScoreLayout score_layout(const cc_problem* p) {
   L.o = off;
   off += align_up(N * p->n_heads_q * p->head_dim * es);
   L.u = off;
-  off += align_up(N * p->hidden * es);
+  if (p->mode != CC_MODE_LAST_LAYER_FUSED) off += align_up(N * p->hidden * es);
   L.lm = off;
   off += lmhead_ws_bytes(p);
   L.total = off;
@@ -236,8 +236,10 @@ cc_status run_attention(const cc_problem* p, const void* q, const cc_kv* kv, int
   return CC_OK;
 }
 
+// LM head over rows u [N][D]; D is the model width unless given (the fused weight's
+// input width Hq*d).
 cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const int32_t* ids,
-                     float* scores, float* lse, void* ws, hipStream_t s) {
+                     float* scores, float* lse, void* ws, hipStream_t s, int D = 0) {
   const int N = n_tokens(p);
   const int vt = lmhead_vocab_tile(p->dtype);
   const size_t n_vt = (p->vocab + vt - 1) / vt;
@@ -253,7 +255,7 @@ cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const
   a.cu_d = p->cu_seqlens_d;
   a.n_seqs = p->n_seqs;
   a.N = N;
-  a.D = p->hidden;
+  a.D = D > 0 ? D : p->hidden;
   a.V = p->vocab;
   a.n_frozen = p->n_frozen;
   CC_HIP(launch_lmhead(a, s));
@@ -429,7 +431,8 @@ cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_
 cc_status cc_score_workspace(const cc_problem* p, size_t* bytes) {
   if (!bytes) return CC_ERR_ARG;
   CC_TRY(check_problem(p));
-  *bytes = p->mode == CC_MODE_LAST_LAYER ? score_layout(p).total : full_layout(p).total;
+  const bool last = p->mode == CC_MODE_LAST_LAYER || p->mode == CC_MODE_LAST_LAYER_FUSED;
+  *bytes = last ? score_layout(p).total : full_layout(p).total;
   return CC_OK;
 }
 
@@ -441,8 +444,11 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   if (p->mode == CC_MODE_LAST_LAYER_H) return score_last_h(p, in, scores, ws, ws_bytes, stream);
   CC_TRY(check_kv(p, &in->kv, 1));
   const int N = n_tokens(p);
-  if (N > 0 && (!in->q || !in->w_o || !in->w_lm || !in->token_ids || !scores)) return CC_ERR_ARG;
-  if (p->dtype == CC_BF16 && (!aligned16(in->q) || !aligned16(in->w_o) || !aligned16(in->w_lm)))
+  const bool fused = p->mode == CC_MODE_LAST_LAYER_FUSED;
+  if (N > 0 && (!in->q || (!fused && !in->w_o) || !in->w_lm || !in->token_ids || !scores))
+    return CC_ERR_ARG;
+  if (p->dtype == CC_BF16 &&
+      (!aligned16(in->q) || (!fused && !aligned16(in->w_o)) || !aligned16(in->w_lm)))
     return CC_ERR_ARG;
   const ScoreLayout L = score_layout(p);
   CC_TRY(check_ws(ws, ws_bytes, L.total));
@@ -451,8 +457,40 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   void* o = at(ws, L.o);
   void* u = at(ws, L.u);
   CC_TRY(run_attention(p, in->q, &in->kv, in->kv.n_layers - 1, o, at(ws, L.attn), s));
-  CC_HIP(launch_linear(p->dtype, o, in->w_o, u, N, p->hidden, p->n_heads_q * p->head_dim, s));
+  const int qdim = p->n_heads_q * p->head_dim;
+  if (fused)   // z = (W_lm W_o) y straight from the attention rows
+    return run_lmhead(p, o, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, qdim);
+  CC_HIP(launch_linear(p->dtype, o, in->w_o, u, N, p->hidden, qdim, s));
   return run_lmhead(p, u, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+}
+
+// ------------------------------------------------------------------ fused LM-head weight
+
+cc_status cc_fuse_wo_lmhead_workspace(int32_t dtype, int32_t hidden, int32_t qdim,
+                                      size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  if (dtype != CC_F32 && dtype != CC_BF16) return CC_ERR_DTYPE;
+  if (hidden < 1 || qdim < 1) return CC_ERR_SHAPE;
+  *bytes = align_up(size_t(hidden) * qdim * esize(dtype));
+  return CC_OK;
+}
+
+cc_status cc_fuse_wo_lmhead(int32_t dtype, const void* w_lm, const void* w_o, void* out,
+                            int32_t vocab, int32_t hidden, int32_t qdim, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (dtype != CC_F32 && dtype != CC_BF16) return CC_ERR_DTYPE;
+  if (vocab < 1 || hidden < 1 || qdim < 1) return CC_ERR_SHAPE;
+  if (!w_lm || !w_o || !out) return CC_ERR_ARG;
+  if (dtype == CC_BF16) {
+    if (hidden % 64 != 0) return CC_ERR_UNSUPPORTED;
+    if (!aligned16(w_lm) || !aligned16(w_o) || !aligned16(out)) return CC_ERR_ARG;
+  }
+  CC_TRY(check_ws(ws, ws_bytes, align_up(size_t(hidden) * qdim * esize(dtype))));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // W_o [hidden][qdim] -> W_o^T [qdim][hidden] (K-contiguous), then out = W_lm (W_o^T)^T
+  CC_HIP(launch_transpose(dtype, w_o, ws, hidden, qdim, s));
+  CC_HIP(launch_linear(dtype, w_lm, ws, out, vocab, qdim, hidden, s));
+  return CC_OK;
 }
 
 // ------------------------------------------------------------------ selection

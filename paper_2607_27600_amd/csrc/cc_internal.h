@@ -90,6 +90,9 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
 // GEMM y[M][N] = x[M][K] w[N][K]^T, bf16 in / bf16 out (or f32 for dtype CC_F32).
 hipError_t launch_linear(int dtype, const void* x, const void* w, void* y, int M, int N, int K,
                          hipStream_t s);
+// out[c][r] = in[r][c], in [rows][cols] (dtype elements).
+hipError_t launch_transpose(int dtype, const void* in, void* out, int rows, int cols,
+                            hipStream_t s);
 
 // LM head with fused log-sum-exp: per (token, vocab tile) partial (max, sumexp) and the
 // target logit, then the combine into scores.

@@ -615,7 +615,40 @@ __global__ __launch_bounds__(CMB_E * CMB_G) void lse_combine(const float2* parti
   }
 }
 
+// out[c][r] = in[r][c] for an in [rows][cols] matrix: 64x64 tiles through LDS (one
+// padding column, so the column reads hit distinct banks).  Used once per model to lay
+// W_o out K-contiguous for the fused LM-head weight.
+template <class T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, T* __restrict__ out,
+                                                        int rows, int cols) {
+  __shared__ T tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) tile[i][tx] = in[int64_t(r) * cols + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) out[int64_t(c) * rows + r] = tile[tx][i];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_transpose(int dtype, const void* in, void* out, int rows, int cols,
+                            hipStream_t s) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const dim3 grid((cols + 63) / 64, (rows + 63) / 64);
+  if (dtype == CC_BF16)
+    hipLaunchKernelGGL(transpose_kernel<u16>, grid, dim3(256), 0, s, static_cast<const u16*>(in),
+                       static_cast<u16*>(out), rows, cols);
+  else
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s,
+                       static_cast<const float*>(in), static_cast<float*>(out), rows, cols);
+  return hipGetLastError();
+}
 
 int lmhead_vocab_tile(int dtype) { return dtype == CC_BF16 ? GBM : FT; }
 

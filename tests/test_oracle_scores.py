@@ -111,6 +111,39 @@ def test_ragged_scores_match_per_sequence():
     np.testing.assert_array_equal(O.last_layer_scores(q, k, v, wo, wl, ids, cu, rows=sub), s[sub])
 
 
+def test_fused_weight_scores_equal_the_two_step_chain():
+    """With queries given, the fast variant's output processing is the bare W_o, so
+    z = W_lm (W_o y) = (W_lm W_o) y: scores through the product weight equal the two-step
+    chain's (fp64 rounding only).  D != Hq*d makes a transposed operand unformable; the
+    square case (D == Hq*d, the usual shapes) would accept one, and the random W_o below
+    would then disagree."""
+    r = np.random.default_rng(17)
+    lens = [6, 1, 9]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    N, hq, hkv, d, V = int(cu[-1]), 4, 2, 8, 60
+    q = r.standard_normal((N, hq, d))
+    k = r.standard_normal((hkv, N, d))
+    v = r.standard_normal((hkv, N, d))
+    ids = r.integers(0, V, N)
+    for D in (24, hq * d):
+        wo = r.standard_normal((D, hq * d)) * 0.2
+        wl = r.standard_normal((V, D)) * 0.2
+        M = O.fused_lmhead_weight(wl, wo)
+        assert M.shape == (V, hq * d)
+        ref = O.last_layer_scores(q, k, v, wo, wl, ids, cu, n_frozen=1)
+        got = O.last_layer_fused_scores(q, k, v, M, ids, cu, n_frozen=1)
+        np.testing.assert_array_equal(np.isinf(got), np.isinf(ref))
+        fin = np.isfinite(ref)
+        np.testing.assert_allclose(got[fin], ref[fin], rtol=1e-12, atol=1e-12)
+    # the product itself, entry by entry on a tiny case
+    wl = r.standard_normal((3, 4))
+    wo = r.standard_normal((4, 5))
+    M = O.fused_lmhead_weight(wl, wo)
+    for a in range(3):
+        for c in range(5):
+            assert M[a, c] == pytest.approx(sum(wl[a, t] * wo[t, c] for t in range(4)), rel=1e-14)
+
+
 def test_uniform_keys_closed_form_score():
     """Uniform keys make attention a suffix mean, so the whole fast-path score has a
     closed form built from reverse cumulative sums and a library logsumexp."""
