@@ -311,6 +311,89 @@ def last_layer_h_scores(h_last, ids, K, V, W, final_norm_w, w_lm, cu_seqlens, n_
 
 
 # ----------------------------------------------------------------------------------
+# LM head on an FP8-quantized model (an implementation variant of the surprise score,
+# Eq. (5); the paper fixes no precision).  FP8 is the OCP E4M3 ("FN") format: sign,
+# 4 exponent bits (bias 7), 3 mantissa bits, subnormals, no infinities, 0x7F / 0xFF NaN,
+# largest finite 448.  Activations u get one scale per row, the LM head one scale for the
+# whole matrix; both are chosen in fp32 so the largest magnitude maps to 448.
+# ----------------------------------------------------------------------------------
+
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    """Value of each E4M3 code (uint8) as float64; NaN for 0x7F / 0xFF."""
+    c = np.asarray(codes, dtype=np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = (c & 7).astype(np.float64)
+    mag = np.where(e == 0, m * 2.0 ** -9, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    mag = np.where((e == 0xF) & ((c & 7) == 7), np.nan, mag)
+    return sign * mag
+
+
+# the 127 non-negative finite values, code 0x00 .. 0x7E, ascending
+_E4M3_POS = e4m3_decode(np.arange(0x7F))
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """Nearest E4M3 code of each value (round to nearest, ties to the even code, i.e. the
+    even mantissa); magnitudes above 448 saturate to 448; -0.0 keeps its sign."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.abs(x)
+    lo = np.clip(np.searchsorted(_E4M3_POS, a, side="right") - 1, 0, 0x7E)   # v[lo] <= a
+    hi = np.minimum(lo + 1, 0x7E)
+    dlo = a - _E4M3_POS[lo]
+    dhi = _E4M3_POS[hi] - a
+    take_hi = (dhi < dlo) | ((dhi == dlo) & (hi != lo) & (hi % 2 == 0))
+    code = np.where(take_hi, hi, lo)
+    code = np.where(a >= E4M3_MAX, 0x7E, code)
+    neg = np.signbit(x)
+    code = np.where(neg, code | 0x80, code)
+    return np.where(np.isnan(x), 0x7F, code).astype(np.uint8)
+
+
+def quantize_fp8(x, per_row: bool = True):
+    """(codes, scale): x ~= decode(codes) * scale.  Per row (or over the whole matrix):
+    amax = max |x|, codes = E4M3(x * (448 / amax)), scale = amax / 448, every step in
+    fp32 as stored (an all-zero row gets codes 0, scale 0)."""
+    x32 = f64(x).astype(np.float32)
+    a = np.abs(x32)
+    amax = a.max(axis=1) if per_row else np.array([a.max()], dtype=np.float32)
+    amax = amax.astype(np.float32)
+    nz = amax > 0
+    inv = np.zeros_like(amax)
+    inv[nz] = np.float32(E4M3_MAX) / amax[nz]
+    scale = (amax / np.float32(E4M3_MAX)).astype(np.float32)
+    y = x32 * (inv[:, None] if per_row else inv[0])
+    return e4m3_encode(y.astype(np.float32)), scale
+
+
+def lmhead_fp8_scores(u, w_codes, w_scale, ids, cu_seqlens, n_frozen=0, rows=None,
+                      vocab_chunk: int = 8192):
+    """Surprise scores (Eq. (5) read as -log P) of rows u [R][D] through an FP8 LM head:
+    u is quantized per row as in quantize_fp8, W_lm is given as E4M3 codes [V][D] with one
+    fp32 scale, and z = (sum over d of the decoded products) * scale_u * scale_w exactly.
+    ``rows`` lists the global row of each u row (all rows by default)."""
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    qu, su = quantize_fp8(u, per_row=True)
+    U = e4m3_decode(qu)
+    R = U.shape[0]
+    rows = np.arange(R) if rows is None else np.asarray(rows, dtype=np.int64)
+    V = w_codes.shape[0]
+    z = np.empty((R, V))
+    for lo in range(0, V, vocab_chunk):
+        hi = min(V, lo + vocab_chunk)
+        z[:, lo:hi] = U @ e4m3_decode(w_codes[lo:hi]).T
+    z *= su.astype(np.float64)[:, None] * float(w_scale)
+    lse = logsumexp_rows(z)
+    ids = np.asarray(ids, dtype=np.int64)
+    s = lse - z[np.arange(R), ids]
+    s[edge_rows(cu, n_frozen)[rows]] = np.inf
+    return s
+
+
+# ----------------------------------------------------------------------------------
 # keep selection and compaction (Sec. 3.2, memory refresh)
 # ----------------------------------------------------------------------------------
 
