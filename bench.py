@@ -24,6 +24,7 @@ if ROOT not in sys.path:
 # MI355X published peaks
 PEAK_BF16_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
+PEAK_FP8_TFLOPS = 5033.2     # dense E4M3 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
 METRIC = "cached tokens scored/sec per refresh; attention TFLOP/s as % of bf16 MFMA peak"
 
 
@@ -347,6 +348,71 @@ def fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len,
                     "attention -> LM head on the product -> select -> compaction"}
 
 
+def fp8_step_timing(args, cc, w, p, cfg, o, u, scores_bf16, ks, seg_start, seg_len, ws_att,
+                    ws_sel, ws_cmp, out_kv, stream, ms_two_step):
+    """The fast-variant step with the LM head on E4M3 codes (one scale for W_lm, one per
+    entry for u, quantized inside the call): kernel time, step time, and how far its
+    scores and keep set are from the bf16 step's."""
+    import torch
+    N, Hq, d, D, V = cfg.n_tokens, cfg.n_heads_q, cfg.head_dim, cfg.hidden, cfg.vocab
+    dev = scores_bf16.device
+    k_keep = ks[0]
+    keep_bf = torch.empty(len(ks) * k_keep, dtype=torch.int32, device=dev)
+    cc.cc_select_keep(scores_bf16, seg_start, seg_len, ks, keep_bf, ws_sel)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    wq, wsc = cc.cc_quantize_fp8("bf16", w.w_lm, per_row=False)
+    ev[0].record(stream)
+    cc.cc_quantize_fp8("bf16", w.w_lm, per_row=False, codes=wq, scale=wsc)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    quant_ms = ev[0].elapsed_time(ev[1])
+    ws8 = torch.empty(cc.cc_lmhead_fp8_workspace(p), dtype=torch.uint8, device=dev)
+    s8 = torch.empty(N, dtype=torch.float32, device=dev)
+    keep8 = torch.empty_like(keep_bf)
+
+    def lm8():
+        cc.cc_lmhead_score_fp8(p, u, wq, wsc, w.ids, s8, workspace=ws8)
+
+    def step8():
+        cc.cc_attention_cc(p, w.q, w.kv, w.cache_layers - 1, o, ws_att)
+        cc.cc_linear("bf16", o.view(N, Hq * d), w.w_o, u)
+        lm8()
+        cc.cc_select_keep(s8, seg_start, seg_len, ks, keep8, ws_sel)
+        cc.cc_compact_kv(p, w.kv, keep8, ks, int(cfg.per_head_select), out=out_kv,
+                         workspace=ws_cmp)
+
+    for _ in range(max(1, args.warmup)):
+        step8()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step8()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev[0].record(stream)
+    for _ in range(args.steps):
+        lm8()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    lm_ms = ev[0].elapsed_time(ev[1]) / args.steps
+    fin = torch.isfinite(scores_bf16)
+    diff = (s8[fin] - scores_bf16[fin]).abs()
+    a = set(keep_bf.cpu().tolist())
+    b = set(keep8.cpu().tolist())
+    flop = 2.0 * N * D * V
+    del wq, ws8
+    return {"ms_per_step": ms, "tokens_per_s": N / (ms * 1e-3),
+            "speedup_vs_bf16_step": ms_two_step / ms, "lmhead_ms": lm_ms,
+            "lmhead_tflops": flop / (lm_ms * 1e-3) / 1e12,
+            "lmhead_frac_fp8_peak": flop / (lm_ms * 1e-3) / 1e12 / PEAK_FP8_TFLOPS,
+            "quantize_w_ms": quant_ms,
+            "score_diff_vs_bf16": {"max_abs": float(diff.max().item()),
+                                   "mean_abs": float(diff.mean().item())},
+            "keep_overlap_vs_bf16": len(a & b) / max(1, len(a)),
+            "note": "W_lm quantized once per model (quantize_w_ms, outside the step); u is "
+                    "quantized per entry inside the LM-head call; lmhead_ms includes that"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -453,6 +519,9 @@ def main():
     # attention -> LM head on the product -> select -> compaction.
     fused = fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len, ws_sel,
                               ws_cmp, out_kv, stream, ms_step)
+    # NEXT-4, low precision: the LM head on E4M3 codes (reported beside the bf16 headline)
+    fp8 = fp8_step_timing(args, cc, w, p, cfg, o, u, scores, ks, seg_start, seg_len, ws_att,
+                          ws_sel, ws_cmp, out_kv, stream, ms_step)
 
     # in-place compaction (what a refresh does to the live cache), timed on its own after
     # the steps: every call moves the same bytes
@@ -513,6 +582,7 @@ def main():
                              "frac_hbm_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "select_sweep": sweep,
         "fused_wo_lmhead": fused,
+        "lmhead_fp8": fp8,
         "breakdown_ms": part_ms,
         "wo_proj_tflops": wo_flop / (part_ms["wo_proj"] * 1e-3) / 1e12,
         "input_generation_s": t_gen,

@@ -220,6 +220,35 @@ cc_status cc_fuse_wo_lmhead(int32_t dtype, const void* w_lm, const void* w_o, vo
 cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_t M,
                     int32_t N, int32_t K, void* stream);
 
+/* ------------------------------------------------------------------ FP8 LM head */
+
+/* Workspace for cc_quantize_fp8 on `rows` rows. */
+cc_status cc_quantize_fp8_workspace(int64_t rows, size_t* bytes);
+
+/* OCP FP8 E4M3 quantization of x [rows][cols] (dtype): per_row = 1 gives each row its own
+ * scale, per_row = 0 one scale for the matrix.  amax = max |x| over the row (matrix),
+ * codes = E4M3(x * (448 / amax)) rounded to nearest even, scale = amax / 448, every step
+ * in fp32; an all-zero row (matrix) gets codes 0 and scale 0.  codes: device uint8
+ * [rows][cols] (4-byte aligned); scale: device float [rows] (per_row) or [1].
+ * cols must be a positive multiple of 4.  A weight preparation for cc_lmhead_score_fp8
+ * (the LM head, one scale); not part of the method (the paper fixes no precision). */
+cc_status cc_quantize_fp8(int32_t dtype, const void* x, int64_t rows, int32_t cols,
+                          int32_t per_row, uint8_t* codes, float* scale, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* Workspace for cc_lmhead_score_fp8. */
+cc_status cc_lmhead_fp8_workspace(const cc_problem* p, size_t* bytes);
+
+/* cc_lmhead_score on an FP8 LM head: u [N][D] (dtype) is quantized per row into the
+ * workspace as in cc_quantize_fp8; w_codes [V][D] are the LM head's E4M3 codes with one
+ * device scale w_scale[0]; the logits are z = (sum_d code products) * scale_u * scale_w,
+ * accumulated in fp32 on the FP8 matrix cores, and the score follows Eq. (5) as in
+ * cc_lmhead_score.  D = p->hidden must be a multiple of 128; w_codes 16-byte aligned. */
+cc_status cc_lmhead_score_fp8(const cc_problem* p, const void* u, const uint8_t* w_codes,
+                              const float* w_scale, const int32_t* token_ids, float* scores,
+                              float* lse, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
 /* ------------------------------------------------------------------ selection */
 
 /* Workspace for cc_select_keep with n_segs segments. */

@@ -353,20 +353,27 @@ def e4m3_encode(x) -> np.ndarray:
     return np.where(np.isnan(x), 0x7F, code).astype(np.uint8)
 
 
-def quantize_fp8(x, per_row: bool = True):
+def quantize_fp8(x, per_row: bool = True, row_chunk: int = 4096):
     """(codes, scale): x ~= decode(codes) * scale.  Per row (or over the whole matrix):
     amax = max |x|, codes = E4M3(x * (448 / amax)), scale = amax / 448, every step in
-    fp32 as stored (an all-zero row gets codes 0, scale 0)."""
-    x32 = f64(x).astype(np.float32)
-    a = np.abs(x32)
-    amax = a.max(axis=1) if per_row else np.array([a.max()], dtype=np.float32)
-    amax = amax.astype(np.float32)
+    fp32 as stored (an all-zero row gets codes 0, scale 0).  Rows are processed in
+    slices only to bound memory; each code depends on its element and amax alone."""
+    R = x.shape[0]
+    amax = np.empty(R, dtype=np.float32)
+    for lo in range(0, R, row_chunk):
+        amax[lo:lo + row_chunk] = np.abs(f64(x[lo:lo + row_chunk]).astype(np.float32)).max(axis=1)
+    if not per_row:
+        amax = np.array([amax.max()], dtype=np.float32)
     nz = amax > 0
     inv = np.zeros_like(amax)
     inv[nz] = np.float32(E4M3_MAX) / amax[nz]
     scale = (amax / np.float32(E4M3_MAX)).astype(np.float32)
-    y = x32 * (inv[:, None] if per_row else inv[0])
-    return e4m3_encode(y.astype(np.float32)), scale
+    codes = np.empty(x.shape, dtype=np.uint8)
+    for lo in range(0, R, row_chunk):
+        x32 = f64(x[lo:lo + row_chunk]).astype(np.float32)
+        f = inv[lo:lo + row_chunk, None] if per_row else inv[0]
+        codes[lo:lo + row_chunk] = e4m3_encode((x32 * f).astype(np.float32))
+    return codes, scale
 
 
 def lmhead_fp8_scores(u, w_codes, w_scale, ids, cu_seqlens, n_frozen=0, rows=None,

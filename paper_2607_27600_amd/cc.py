@@ -29,7 +29,8 @@ EXPORTED = [
     "cc_attention_cc", "cc_lmhead_workspace", "cc_lmhead_score", "cc_linear",
     "cc_select_workspace", "cc_select_keep", "cc_compact_workspace", "cc_compact_kv",
     "cc_compact_rows_workspace", "cc_compact_rows", "cc_fuse_wo_lmhead_workspace",
-    "cc_fuse_wo_lmhead",
+    "cc_fuse_wo_lmhead", "cc_quantize_fp8_workspace", "cc_quantize_fp8",
+    "cc_lmhead_fp8_workspace", "cc_lmhead_score_fp8",
 ]
 
 _c_void_p = ctypes.c_void_p
@@ -87,6 +88,13 @@ def _load():
                                  _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p]),
         "cc_linear": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32, _c_void_p]),
         "cc_fuse_wo_lmhead_workspace": (st, [_i32, _i32, _i32, sz]),
+        "cc_quantize_fp8_workspace": (st, [_i64, sz]),
+        "cc_quantize_fp8": (st, [_i32, _c_void_p, _i64, _i32, _i32, _c_void_p, _c_void_p,
+                                 _c_void_p, ctypes.c_size_t, _c_void_p]),
+        "cc_lmhead_fp8_workspace": (st, [P(c_problem), sz]),
+        "cc_lmhead_score_fp8": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                     _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
+                                     _c_void_p]),
         "cc_fuse_wo_lmhead": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32,
                                    _c_void_p, ctypes.c_size_t, _c_void_p]),
         "cc_select_workspace": (st, [_i32, sz]),
@@ -317,6 +325,43 @@ def cc_fuse_wo_lmhead(dtype: str, w_lm: torch.Tensor, w_o: torch.Tensor,
                                   _ptr(out), V, D, Q, _ptr(workspace), workspace.numel(),
                                   _stream(stream)), "cc_fuse_wo_lmhead")
     return out
+
+
+def cc_quantize_fp8_workspace(rows: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib.cc_quantize_fp8_workspace(rows, ctypes.byref(n)), "cc_quantize_fp8_workspace")
+    return n.value
+
+
+def cc_quantize_fp8(dtype: str, x: torch.Tensor, per_row: bool, codes=None, scale=None,
+                    workspace=None, stream=None):
+    """E4M3 codes (uint8, x's shape) and fp32 scales ([rows], or [1] for the matrix)."""
+    rows, cols = x.shape
+    if codes is None:
+        codes = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty(rows if per_row else 1, dtype=torch.float32, device=x.device)
+    if workspace is None:
+        workspace = _workspace(cc_quantize_fp8_workspace(rows), x.device)
+    _check(_lib.cc_quantize_fp8({"f32": CC_F32, "bf16": CC_BF16}[dtype], _ptr(x), rows, cols,
+                                int(per_row), _ptr(codes), _ptr(scale), _ptr(workspace),
+                                workspace.numel(), _stream(stream)), "cc_quantize_fp8")
+    return codes, scale
+
+
+def cc_lmhead_fp8_workspace(p: Problem) -> int:
+    return _query(_lib.cc_lmhead_fp8_workspace, ctypes.byref(p.struct))
+
+
+def cc_lmhead_score_fp8(p: Problem, u: torch.Tensor, w_codes: torch.Tensor, w_scale: torch.Tensor,
+                        token_ids: torch.Tensor, scores: torch.Tensor,
+                        lse: Optional[torch.Tensor] = None, workspace=None, stream=None):
+    if workspace is None:
+        workspace = _workspace(cc_lmhead_fp8_workspace(p), p.device)
+    _check(_lib.cc_lmhead_score_fp8(ctypes.byref(p.struct), _ptr(u), _ptr(w_codes), _ptr(w_scale),
+                                    _ptr(token_ids), _ptr(scores), _ptr(lse), _ptr(workspace),
+                                    workspace.numel(), _stream(stream)), "cc_lmhead_score_fp8")
+    return scores
 
 
 def cc_linear(dtype: str, x: torch.Tensor, w: torch.Tensor, y: torch.Tensor, stream=None):

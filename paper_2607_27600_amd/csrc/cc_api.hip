@@ -493,6 +493,94 @@ cc_status cc_fuse_wo_lmhead(int32_t dtype, const void* w_lm, const void* w_o, vo
   return CC_OK;
 }
 
+// ------------------------------------------------------------------ FP8 LM head
+
+cc_status cc_quantize_fp8_workspace(int64_t rows, size_t* bytes) {
+  if (!bytes || rows < 0) return CC_ERR_ARG;
+  *bytes = align_up(size_t(rows + 1) * sizeof(float));
+  return CC_OK;
+}
+
+cc_status cc_quantize_fp8(int32_t dtype, const void* x, int64_t rows, int32_t cols,
+                          int32_t per_row, uint8_t* codes, float* scale, void* ws,
+                          size_t ws_bytes, void* stream) {
+  if (dtype != CC_F32 && dtype != CC_BF16) return CC_ERR_DTYPE;
+  if (rows < 0 || rows > INT32_MAX || cols < 4 || cols % 4 != 0) return CC_ERR_SHAPE;
+  if (per_row != 0 && per_row != 1) return CC_ERR_ARG;
+  if (rows == 0) return CC_OK;
+  if (!x || !codes || !scale) return CC_ERR_ARG;
+  if ((reinterpret_cast<uintptr_t>(codes) & 3u) != 0) return CC_ERR_ARG;
+  CC_TRY(check_ws(ws, ws_bytes, align_up(size_t(rows + 1) * sizeof(float))));
+  CC_HIP(launch_quantize_e4m3(dtype, x, rows, cols, per_row, codes, scale,
+                              static_cast<float*>(ws), static_cast<hipStream_t>(stream)));
+  return CC_OK;
+}
+
+namespace {
+struct Fp8Layout {
+  size_t uq, su, amax, partial, target, total;
+};
+Fp8Layout fp8_layout(const cc_problem* p) {
+  Fp8Layout L;
+  const size_t N = n_tokens(p), D = p->hidden;
+  const size_t n_vt = (p->vocab + 255) / 256;
+  size_t off = 0;
+  L.uq = off;
+  off += align_up(N * D);
+  L.su = off;
+  off += align_up(N * sizeof(float));
+  L.amax = off;
+  off += align_up((N + 1) * sizeof(float));
+  L.partial = off;
+  off += align_up(n_vt * N * sizeof(float2));
+  L.target = off;
+  off += align_up(N * sizeof(float));
+  L.total = off;
+  return L;
+}
+}  // namespace
+
+cc_status cc_lmhead_fp8_workspace(const cc_problem* p, size_t* bytes) {
+  if (!bytes) return CC_ERR_ARG;
+  CC_TRY(check_problem(p));
+  *bytes = fp8_layout(p).total;
+  return CC_OK;
+}
+
+cc_status cc_lmhead_score_fp8(const cc_problem* p, const void* u, const uint8_t* w_codes,
+                              const float* w_scale, const int32_t* token_ids, float* scores,
+                              float* lse, void* ws, size_t ws_bytes, void* stream) {
+  CC_TRY(check_problem(p));
+  if (p->hidden % 128 != 0) return CC_ERR_UNSUPPORTED;
+  const int N = n_tokens(p);
+  if (N > 0 && (!u || !w_codes || !w_scale || !token_ids || !scores)) return CC_ERR_ARG;
+  if (N > 0 && !aligned16(w_codes)) return CC_ERR_ARG;
+  const Fp8Layout L = fp8_layout(p);
+  CC_TRY(check_ws(ws, ws_bytes, L.total));
+  if (N == 0) return CC_OK;
+  LmHeadFp8Launch a;
+  a.dtype = p->dtype;
+  a.u = u;
+  a.wq = w_codes;
+  a.sw = w_scale;
+  a.ids = token_ids;
+  a.scores = scores;
+  a.lse = lse;
+  a.uq = reinterpret_cast<uint8_t*>(at(ws, L.uq));
+  a.su = reinterpret_cast<float*>(at(ws, L.su));
+  a.amax_ws = reinterpret_cast<float*>(at(ws, L.amax));
+  a.partial = reinterpret_cast<float2*>(at(ws, L.partial));
+  a.target = reinterpret_cast<float*>(at(ws, L.target));
+  a.cu_d = p->cu_seqlens_d;
+  a.n_seqs = p->n_seqs;
+  a.N = N;
+  a.D = p->hidden;
+  a.V = p->vocab;
+  a.n_frozen = p->n_frozen;
+  CC_HIP(launch_lmhead_fp8(a, static_cast<hipStream_t>(stream)));
+  return CC_OK;
+}
+
 // ------------------------------------------------------------------ selection
 
 cc_status cc_select_workspace(int32_t n_segs, size_t* bytes) {

@@ -113,6 +113,32 @@ struct LmHeadLaunch {
 int lmhead_vocab_tile(int dtype);
 hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s);
 
+// FP8 LM head: u (dtype) quantized per row into uq / su, then the E4M3 GEMM with the LSE
+// epilogue on the scaled logits, the target logits and the combine.
+struct LmHeadFp8Launch {
+  int dtype;             // of u
+  const void* u;         // [N][D]
+  const uint8_t* wq;     // [V][D] E4M3 codes
+  const float* sw;       // [1] device scale of wq
+  const int32_t* ids;    // [N]
+  float* scores;         // [N]
+  float* lse;            // [N] or null
+  uint8_t* uq;           // workspace [N][D]
+  float* su;             // workspace [N]
+  float* amax_ws;        // workspace [N]
+  float2* partial;       // workspace [n_vtiles][N]
+  float* target;         // workspace [N]
+  const int32_t* cu_d;
+  int n_seqs;
+  int N, D, V;
+  int n_frozen;
+};
+hipError_t launch_lmhead_fp8(const LmHeadFp8Launch& a, hipStream_t s);
+// E4M3 codes and scales of x [rows][cols] (dtype), per row or one for the matrix;
+// amax_ws holds rows + 1 floats.
+hipError_t launch_quantize_e4m3(int dtype, const void* x, int64_t rows, int cols, int per_row,
+                                uint8_t* q, float* scale, float* amax_ws, hipStream_t s);
+
 // Keep selection: one workgroup per segment.
 struct SelSeg {
   int64_t start;   // score offset

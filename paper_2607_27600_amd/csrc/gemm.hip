@@ -65,11 +65,17 @@ struct EpiStore {
 // the workgroup's 256 vocabulary rows.  The whole epilogue runs while the matrix cores
 // idle, so it is kept to one max and one exp-accumulate per logit; only workgroups on the
 // vocabulary edge take the masked variant.
+// An FP8 LM head passes the dequantization scales: the logit is acc * sw * su[n]
+// (su per entry, sw for the whole matrix); without them the factor is 1 and the
+// arithmetic is unchanged.
 struct EpiLse {
   float2* partial;
+  const float* su = nullptr;   // [N] per-entry scale, or null
+  const float* sw = nullptr;   // [1] matrix scale (device), with su
   template <bool EDGE>
   __device__ __forceinline__ void reduce(const f32x16 (&acc)[GMB][GNB], int M, int m0w, int hi,
-                                         float (&mx)[GNB], float (&sm)[GNB]) const {
+                                         const float (&f)[GNB], float (&mx)[GNB],
+                                         float (&sm)[GNB]) const {
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) mx[nb] = -INFINITY;
 #pragma unroll
@@ -81,11 +87,14 @@ struct EpiLse {
         for (int nb = 0; nb < GNB; ++nb)
           if (ok) mx[nb] = fmaxf(mx[nb], acc[mb][nb][e]);
       }
-    float mc[GNB];
+    float mc[GNB], c[GNB];
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
-      // a lane whose rows are all past the edge keeps max = -inf and sum = 0
+      // logits are acc * f (f >= 0), so their max is mx * f; a lane whose rows are all
+      // past the edge keeps max = -inf and sum = 0
+      if (mx[nb] != -INFINITY) mx[nb] *= f[nb];
       mc[nb] = mx[nb] == -INFINITY ? 0.f : mx[nb] * kLog2e;
+      c[nb] = kLog2e * f[nb];
       sm[nb] = 0.f;
     }
 #pragma unroll
@@ -95,7 +104,7 @@ struct EpiLse {
         const bool ok = !EDGE || (m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3) < M);
 #pragma unroll
         for (int nb = 0; nb < GNB; ++nb)
-          if (ok) sm[nb] += fast_exp2(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
+          if (ok) sm[nb] += fast_exp2(fmaf(acc[mb][nb][e], c[nb], -mc[nb]));
       }
   }
 
@@ -105,11 +114,15 @@ struct EpiLse {
     const int wave = threadIdx.x >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
+    float f[GNB];
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb)
+      f[nb] = su ? sw[0] * su[min(n0w + nb * 32 + col, g.N - 1)] : 1.f;
     float mx[GNB], sm[GNB];
     if (tm * GBM + GBM <= g.M)
-      reduce<false>(acc, g.M, m0w, hi, mx, sm);
+      reduce<false>(acc, g.M, m0w, hi, f, mx, sm);
     else
-      reduce<true>(acc, g.M, m0w, hi, mx, sm);
+      reduce<true>(acc, g.M, m0w, hi, f, mx, sm);
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
       // combine the two lane halves (rows 4*hi..)
@@ -415,6 +428,210 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds0);
+}
+
+// ------------------------------------------------------------------ FP8 path
+// The same contraction on OCP E4M3 codes (one byte per element) with the gfx950
+// 32x32x64 FP8 MFMA (unit block scales, so it multiplies the codes' values exactly and
+// accumulates in fp32).  Rows of K bytes are moved as K/2 16-bit units: the loader, the
+// LDS stages and their swizzle are those of the bf16 kernel, so one k-tile holds 128
+// codes per row; a k-step of 64 codes takes 32 bytes per lane (two 16-byte chunks).
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x16 mfma_fp8(i32x8 a, i32x8 b, f32x16 c) {
+  // operand formats 0 (E4M3), block scales 127 (2^0)
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+}
+
+template <class Epi>
+__global__ __launch_bounds__(GNT, 1) void gemm_tn_fp8(GemmArgs g, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) u16 lds0[STAGE];
+  __shared__ __attribute__((aligned(1024))) u16 lds1[STAGE];
+  int tm, tn;
+  tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+  const int m0 = tm * GBM, n0 = tn * GBN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int hi = lane >> 5, col = lane & 31;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  const u16* ga[LPW];
+  const u16* gb[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int r = (wave * LPW + j) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
+    ga[j] = g.A + int64_t(min(m0 + r, g.M - 1)) * g.lda + c * 8;
+    gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8;
+  }
+  auto issue_half = [&](u16* stage, int k0, int h) {
+    u16* base = stage + wave * LPW * 512 + h * GBM * GBK;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      __builtin_amdgcn_global_load_lds((global_void*)((h ? gb[j] : ga[j]) + k0),
+                                       (lds_void*)(base + j * 512), 16, 0, 0);
+  };
+  // k-step ks (codes 64ks .. 64ks+63 of the tile): lane half hi takes codes 32hi .. +31,
+  // i.e. 16-byte chunks 4ks + 2hi and 4ks + 2hi + 1 of its row
+  auto frag = [&](const u16* S, int r, int ks) {
+    const int c0 = 4 * ks + 2 * hi, sw = (r >> 1) & 7;
+    const uint4 x = ld16(S + r * GBK + ((c0 ^ sw) * 8));
+    const uint4 y = ld16(S + r * GBK + (((c0 + 1) ^ sw) * 8));
+    return i32x8{int(x.x), int(x.y), int(x.z), int(x.w), int(y.x), int(y.y), int(y.z), int(y.w)};
+  };
+  f32x16 acc[GMB][GNB];
+#pragma unroll
+  for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = f32x16{};
+  const int nk = g.K / GBK;
+  // Fragments: fa holds one k-step's A fragments and is refilled block by block as soon
+  // as a block's last MFMA is issued; B fragments are double buffered.  This keeps the
+  // operands at 64 registers (two full sets would spill).
+  i32x8 fa[GMB], fb0[GNB], fb1[GNB];
+  auto rowA = [&](int mb) { return wm * GTM + mb * 32 + col; };
+  auto rowB = [&](int nb) { return GBM + wn * GTN + nb * 32 + col; };
+  // One k-step: MFMAs on (fa, fbc); the next k-step's fragments come from stage Sn at
+  // k-step ksn; `dma` issues this step's direct loads, one after every other MFMA.
+  auto kstep = [&](const i32x8 (&fbc)[GNB], i32x8 (&fbn)[GNB], const u16* Sn, int ksn,
+                   auto dma) {
+#pragma unroll
+    for (int i = 0; i < GMB * GNB; ++i) {
+      const int mb = i / GNB, nb = i % GNB;
+      acc[mb][nb] = mfma_fp8(fa[mb], fbc[nb], acc[mb][nb]);
+      if (i < GNB) fbn[i] = frag(Sn, rowB(i), ksn);
+      if (nb == GNB - 1) fa[mb] = frag(Sn, rowA(mb), ksn);
+      if ((i & 1) == 0) dma(i >> 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto no_dma = [](int) {};
+  // one k-tile from `cur`: k-step 0 carries the B half of `nxt` (k-tile kt+1); after the
+  // barrier that frees `cur`, k-step 1 refills its A half with k-tile kt+2
+  auto tile = [&](const u16* cur, u16* nxt, int kt) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int kb = min(kt + 1, nk - 1) * GBK, ka = min(kt + 2, nk - 1) * GBK;
+    u16* bdst = nxt + wave * LPW * 512 + GBM * GBK;
+    kstep(fb0, fb1, cur, 1, [&](int j) {
+      __builtin_amdgcn_global_load_lds((global_void*)(gb[j] + kb), (lds_void*)(bdst + j * 512),
+                                       16, 0, 0);
+    });
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    u16* adst = const_cast<u16*>(cur) + wave * LPW * 512;
+    kstep(fb1, fb0, nxt, 0, [&](int j) {
+      __builtin_amdgcn_global_load_lds((global_void*)(ga[j] + ka), (lds_void*)(adst + j * 512),
+                                       16, 0, 0);
+    });
+  };
+  (void)no_dma;
+  issue_half(lds0, 0, 0);
+  issue_half(lds0, 0, 1);
+  issue_half(lds1, min(1, nk - 1) * GBK, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < GMB; ++mb) fa[mb] = frag(lds0, rowA(mb), 0);
+#pragma unroll
+  for (int nb = 0; nb < GNB; ++nb) fb0[nb] = frag(lds0, rowB(nb), 0);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    tile(lds0, lds1, kt);
+    tile(lds1, lds0, kt + 1);
+  }
+  if (kt < nk) tile(lds0, lds1, kt);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds0);
+}
+
+// Per-row E4M3 quantization: amax = max |x|, codes = E4M3(x * (448 / amax)) rounded to
+// nearest even by the conversion instruction, scale = amax / 448 (fp32 throughout; an
+// all-zero row gives codes 0 and scale 0).  One workgroup per row; a given amax (one for
+// the whole matrix) replaces the row's own.
+template <class T>
+__device__ __forceinline__ float ldx(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float ldx<u16>(const u16* p, int64_t i) { return bf2f(p[i]); }
+template <>
+__device__ __forceinline__ float ldx<float>(const float* p, int64_t i) { return p[i]; }
+
+__device__ __forceinline__ float block_max_256(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  return v;
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void row_amax_kernel(const T* __restrict__ x, int cols,
+                                                       float* __restrict__ amax) {
+  __shared__ float red[4];
+  const T* row = x + int64_t(blockIdx.x) * cols;
+  float m = 0.f;
+  for (int c = threadIdx.x; c < cols; c += 256) m = fmaxf(m, fabsf(ldx<T>(row, c)));
+  m = block_max_256(m, red);
+  if (threadIdx.x == 0) amax[blockIdx.x] = m;
+}
+
+// max over n values into out[0] (one workgroup)
+__global__ __launch_bounds__(256) void max_reduce_kernel(const float* __restrict__ v, int64_t n,
+                                                         float* __restrict__ out) {
+  __shared__ float red[4];
+  float m = 0.f;
+  for (int64_t i = threadIdx.x; i < n; i += 256) m = fmaxf(m, v[i]);
+  m = block_max_256(m, red);
+  if (threadIdx.x == 0) out[0] = m;
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void quantize_e4m3_kernel(const T* __restrict__ x, int cols,
+                                                            const float* __restrict__ amax_in,
+                                                            int per_row, uint8_t* __restrict__ q,
+                                                            float* __restrict__ scale) {
+  const int64_t r = blockIdx.x;
+  const float amax = amax_in[per_row ? r : 0];
+  const float inv = amax > 0.f ? 448.f / amax : 0.f;
+  if (threadIdx.x == 0 && (per_row || r == 0)) scale[per_row ? r : 0] = amax / 448.f;
+  const T* row = x + r * cols;
+  uint32_t* out = reinterpret_cast<uint32_t*>(q + r * cols);
+  for (int c = threadIdx.x * 4; c < cols; c += 1024) {
+    const float a = ldx<T>(row, c) * inv, b = ldx<T>(row, c + 1) * inv;
+    const float d = ldx<T>(row, c + 2) * inv, e = ldx<T>(row, c + 3) * inv;
+    int v = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+    v = __builtin_amdgcn_cvt_pk_fp8_f32(d, e, v, true);
+    out[c >> 2] = uint32_t(v);
+  }
+}
+
+// z[x_n] of the FP8 head: one wave per entry, the decoded codes' dot product times the
+// two scales
+__global__ __launch_bounds__(256) void target_logit_fp8(const uint8_t* __restrict__ uq,
+                                                        const uint8_t* __restrict__ wq,
+                                                        const float* __restrict__ su,
+                                                        const float* __restrict__ sw,
+                                                        const int32_t* __restrict__ ids,
+                                                        float* __restrict__ target, int N, int D) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const uint32_t* ur = reinterpret_cast<const uint32_t*>(uq + int64_t(n) * D);
+  const uint32_t* wr = reinterpret_cast<const uint32_t*>(wq + int64_t(ids[n]) * D);
+  float acc = 0.f;
+  for (int i = lane; i < D / 4; i += 64) {
+    const int a = int(ur[i]), b = int(wr[i]);
+    const auto a0 = __builtin_amdgcn_cvt_pk_f32_fp8(a, false), a1 = __builtin_amdgcn_cvt_pk_f32_fp8(a, true);
+    const auto b0 = __builtin_amdgcn_cvt_pk_f32_fp8(b, false), b1 = __builtin_amdgcn_cvt_pk_f32_fp8(b, true);
+    acc = fmaf(a0[0], b0[0], acc);
+    acc = fmaf(a0[1], b0[1], acc);
+    acc = fmaf(a1[0], b1[0], acc);
+    acc = fmaf(a1[1], b1[1], acc);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) target[n] = acc * su[n] * sw[0];
 }
 
 // ------------------------------------------------------------------ fp32 path
@@ -728,6 +945,57 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
   hipLaunchKernelGGL(lse_combine, dim3((a.N + CMB_E - 1) / CMB_E), dim3(CMB_E * CMB_G), 0, s,
                      a.partial, n_vt,
                      a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores, a.lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_e4m3(int dtype, const void* x, int64_t rows, int cols, int per_row,
+                                uint8_t* q, float* scale, float* amax_ws, hipStream_t s) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  if (dtype == CC_BF16)
+    hipLaunchKernelGGL(row_amax_kernel<u16>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const u16*>(x), cols, amax_ws);
+  else
+    hipLaunchKernelGGL(row_amax_kernel<float>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const float*>(x), cols, amax_ws);
+  const float* am = amax_ws;
+  if (!per_row) {
+    hipLaunchKernelGGL(max_reduce_kernel, dim3(1), dim3(256), 0, s, amax_ws, rows, amax_ws + rows);
+    am = amax_ws + rows;
+  }
+  if (dtype == CC_BF16)
+    hipLaunchKernelGGL(quantize_e4m3_kernel<u16>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const u16*>(x), cols, am, per_row, q, scale);
+  else
+    hipLaunchKernelGGL(quantize_e4m3_kernel<float>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const float*>(x), cols, am, per_row, q, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_lmhead_fp8(const LmHeadFp8Launch& a, hipStream_t s) {
+  if (a.N == 0) return hipSuccess;
+  hipError_t err = launch_quantize_e4m3(a.dtype, a.u, a.N, a.D, 1, a.uq, a.su, a.amax_ws, s);
+  if (err != hipSuccess) return err;
+  GemmArgs g;
+  g.A2 = nullptr;
+  g.A = reinterpret_cast<const u16*>(a.wq);   // rows of D codes = D/2 16-bit units
+  g.B = reinterpret_cast<const u16*>(a.uq);
+  g.M = a.V;
+  g.N = a.N;
+  g.K = a.D / 2;
+  g.lda = a.D / 2;
+  g.ldb = a.D / 2;
+  g.tiles_n = (a.N + GBN - 1) / GBN;
+  const int n_vt = (a.V + GBM - 1) / GBM;
+  g.tiles_m = n_vt;
+  EpiLse e{a.partial, a.su, a.sw};
+  hipLaunchKernelGGL(gemm_tn_fp8<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  hipLaunchKernelGGL(target_logit_fp8, dim3((a.N + 3) / 4), dim3(256), 0, s, a.uq, a.wq, a.su,
+                     a.sw, a.ids, a.target, a.N, a.D);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  hipLaunchKernelGGL(lse_combine, dim3((a.N + CMB_E - 1) / CMB_E), dim3(CMB_E * CMB_G), 0, s,
+                     a.partial, n_vt, a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores,
+                     a.lse);
   return hipGetLastError();
 }
 

@@ -1,0 +1,130 @@
+"""GPU parity of the FP8 LM head (cc_quantize_fp8, cc_lmhead_score_fp8) against the
+oracle's FP8 reference: E4M3 codes and scales bit for bit (the quantization decides
+integers, both sides in fp32), and the surprise scores (Eq. (5)) of the quantized model
+within the FP8 matrix cores' accumulation error.  The FP8 scores' distance from the bf16
+model's is printed for information (it is the quantization error, not a parity bar)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cc_oracle as O
+from synth import configs as C
+from synth import gen
+from tests.gpu_util import dev
+
+pytestmark = pytest.mark.gpu
+
+# Against the quantized model's exact scores only fp32 accumulation (matrix cores, then the
+# log-sum-exp) separates the two: measured max |error| 2.5e-6 at 256-wide rows and 1.4e-6 at
+# the 8B head; the bar keeps a 40x margin.
+FP8_ATOL, FP8_RTOL = 1e-4, 1e-5
+
+
+def _rows(r, R, Cn, spread=True):
+    x = r.standard_normal((R, Cn)).astype(np.float32)
+    if spread:
+        x *= np.logspace(-2, 2, R, dtype=np.float32)[:, None]
+    return x
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("per_row", [True, False])
+def test_quantize_codes_and_scales_exact(dtype, per_row):
+    from paper_2607_27600_amd import cc
+    print(f"[quantize] {dtype} per_row={per_row}", flush=True)
+    r = np.random.default_rng(3 + per_row)
+    x = _rows(r, 37, 260)
+    x[5] = 0.0
+    x[7, 11] = 1000.0                     # one outlier row
+    if dtype == "bf16":
+        x = gen.f32_to_bf16_bits(x)
+    codes, scale = cc.cc_quantize_fp8(dtype, dev(x), per_row)
+    torch.cuda.synchronize()
+    c_ref, s_ref = O.quantize_fp8(x, per_row=per_row)
+    np.testing.assert_array_equal(codes.cpu().numpy(), c_ref)
+    np.testing.assert_array_equal(scale.cpu().numpy(), s_ref)
+
+
+def _fp8_case(N_lens, D, V, n_frozen, seed):
+    from paper_2607_27600_amd import cc
+    r = np.random.default_rng(seed)
+    cu = np.concatenate([[0], np.cumsum(N_lens)]).astype(np.int32)
+    N = int(cu[-1])
+    u = gen.f32_to_bf16_bits(r.standard_normal((N, D)).astype(np.float32))
+    w = gen.f32_to_bf16_bits((0.05 * r.standard_normal((V, D))).astype(np.float32))
+    ids = r.integers(0, V, N).astype(np.int32)
+    wc, ws = cc.cc_quantize_fp8("bf16", dev(w), per_row=False)
+    p = cc.problem(dtype="bf16", cu_seqlens=cu.tolist(), n_heads_q=1, n_heads_kv=1,
+                   head_dim=128, hidden=D, vocab=V, n_frozen=n_frozen)
+    scores = torch.full((N,), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score_fp8(p, dev(u), wc, ws, dev(ids), scores, lse)
+    torch.cuda.synchronize()
+    wc_ref, ws_ref = O.quantize_fp8(w, per_row=False)
+    np.testing.assert_array_equal(wc.cpu().numpy(), wc_ref)
+    return u, w, ids, cu, wc_ref, ws_ref, scores.cpu().numpy()
+
+
+def test_lmhead_fp8_matches_quantized_oracle():
+    lens = (5, 1, 294)
+    u, w, ids, cu, wc, ws, got = _fp8_case(lens, 256, 1000, 2, 11)
+    ref = O.lmhead_fp8_scores(u, wc, ws[0], ids, cu, n_frozen=2)
+    fin = np.isfinite(ref)
+    err = np.abs(got[fin] - ref[fin])
+    print(f"[fp8 lmhead] vs quantized oracle: max abs {err.max():.3e}", flush=True)
+    np.testing.assert_array_equal(np.isinf(got), np.isinf(ref))
+    assert np.all(np.abs(got[fin] - ref[fin]) <= FP8_ATOL + FP8_RTOL * np.abs(ref[fin]))
+    # distance from the unquantized (bf16 inputs, exact arithmetic) scores: information
+    s_bf, _, _ = O.surprise(O.f64(u), w, ids)
+    d = np.abs(got[fin] - s_bf[fin])
+    print(f"[fp8 lmhead] vs bf16 model: max {d.max():.3e} mean {d.mean():.3e}", flush=True)
+    assert d.max() < 0.5
+
+
+def test_lmhead_fp8_zero_head_gives_ln_vocab():
+    from paper_2607_27600_amd import cc
+    N, D, V = 64, 128, 5000
+    u = gen.f32_to_bf16_bits(np.random.default_rng(2).standard_normal((N, D)).astype(np.float32))
+    w = torch.zeros((V, D), dtype=torch.bfloat16, device="cuda")
+    wc, ws = cc.cc_quantize_fp8("bf16", w, per_row=False)
+    p = cc.problem(dtype="bf16", cu_seqlens=[0, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
+                   hidden=D, vocab=V)
+    scores = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score_fp8(p, dev(u), wc, ws, torch.arange(N, dtype=torch.int32, device="cuda"),
+                           scores)
+    torch.cuda.synchronize()
+    s = scores.cpu().numpy().astype(np.float64)
+    assert s[-1] == np.inf
+    np.testing.assert_allclose(s[:-1], np.log(V), rtol=0, atol=1e-5)
+
+
+@pytest.mark.slow
+def test_lmhead_fp8_c2_shape_sampled():
+    """Llama-3-8B LM head (V 128256, D 4096) over 4096 entries; 48 sampled rows checked
+    against the quantized oracle (codes of the whole head compared first)."""
+    from paper_2607_27600_amd import cc
+    cfg = C.C2
+    print("[fp8 lmhead] C2 shape", flush=True)
+    N, D, V = cfg.n_tokens, cfg.hidden, cfg.vocab
+    r = np.random.default_rng(21)
+    u = gen.f32_to_bf16_bits(r.standard_normal((N, D)).astype(np.float32))
+    w = gen.normal_bf16(0, 3, (V, D), 0.02)
+    ids = r.integers(0, V, N).astype(np.int32)
+    wd = dev(w)
+    wc, ws = cc.cc_quantize_fp8("bf16", wd, per_row=False)
+    p = cc.problem(dtype="bf16", cu_seqlens=[0, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
+                   hidden=D, vocab=V)
+    scores = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score_fp8(p, dev(u), wc, ws, dev(ids), scores)
+    torch.cuda.synchronize()
+    wc_ref, ws_ref = O.quantize_fp8(w, per_row=False)
+    assert np.array_equal(ws.cpu().numpy(), ws_ref)
+    assert np.array_equal(wc.cpu().numpy(), wc_ref), "E4M3 codes of the LM head differ"
+    rows = C.sample_rows(cfg, count=48)
+    ref = O.lmhead_fp8_scores(u[rows], wc_ref, ws_ref[0], ids[rows], [0, N], rows=rows)
+    got = scores.cpu().numpy()[rows]
+    np.testing.assert_array_equal(np.isinf(got), np.isinf(ref))
+    fin = np.isfinite(ref)
+    err = np.abs(got[fin] - ref[fin])
+    print(f"[fp8 lmhead] C2 sampled: max abs {err.max():.3e}", flush=True)
+    assert np.all(err <= FP8_ATOL + FP8_RTOL * np.abs(ref[fin]))
