@@ -228,8 +228,9 @@ cc_status cc_quantize_fp8_workspace(int64_t rows, size_t* bytes);
 /* OCP FP8 E4M3 quantization of x [rows][cols] (dtype): per_row = 1 gives each row its own
  * scale, per_row = 0 one scale for the matrix.  amax = max |x| over the row (matrix),
  * codes = E4M3(x * (448 / amax)) rounded to nearest even, scale = amax / 448, every step
- * in fp32; an all-zero row (matrix) gets codes 0 and scale 0.  codes: device uint8
- * [rows][cols] (4-byte aligned); scale: device float [rows] (per_row) or [1].
+ * in fp32; an all-zero row (matrix) gets codes 0 and scale 0.  x aligned to four
+ * elements; codes: device uint8 [rows][cols] (4-byte aligned); scale: device float
+ * [rows] (per_row) or [1].
  * cols must be a positive multiple of 4.  A weight preparation for cc_lmhead_score_fp8
  * (the LM head, one scale); not part of the method (the paper fixes no precision). */
 cc_status cc_quantize_fp8(int32_t dtype, const void* x, int64_t rows, int32_t cols,

@@ -510,6 +510,7 @@ cc_status cc_quantize_fp8(int32_t dtype, const void* x, int64_t rows, int32_t co
   if (rows == 0) return CC_OK;
   if (!x || !codes || !scale) return CC_ERR_ARG;
   if ((reinterpret_cast<uintptr_t>(codes) & 3u) != 0) return CC_ERR_ARG;
+  if ((reinterpret_cast<uintptr_t>(x) & uintptr_t(4 * esize(dtype) - 1)) != 0) return CC_ERR_ARG;
   CC_TRY(check_ws(ws, ws_bytes, align_up(size_t(rows + 1) * sizeof(float))));
   CC_HIP(launch_quantize_e4m3(dtype, x, rows, cols, per_row, codes, scale,
                               static_cast<float*>(ws), static_cast<hipStream_t>(stream)));
@@ -555,6 +556,8 @@ cc_status cc_lmhead_score_fp8(const cc_problem* p, const void* u, const uint8_t*
   const int N = n_tokens(p);
   if (N > 0 && (!u || !w_codes || !w_scale || !token_ids || !scores)) return CC_ERR_ARG;
   if (N > 0 && !aligned16(w_codes)) return CC_ERR_ARG;
+  if (N > 0 && (reinterpret_cast<uintptr_t>(u) & uintptr_t(4 * esize(p->dtype) - 1)) != 0)
+    return CC_ERR_ARG;
   const Fp8Layout L = fp8_layout(p);
   CC_TRY(check_ws(ws, ws_bytes, L.total));
   if (N == 0) return CC_OK;

@@ -544,16 +544,26 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_fp8(GemmArgs g, Epi epi) {
   epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds0);
 }
 
-// Per-row E4M3 quantization: amax = max |x|, codes = E4M3(x * (448 / amax)) rounded to
-// nearest even by the conversion instruction, scale = amax / 448 (fp32 throughout; an
-// all-zero row gives codes 0 and scale 0).  One workgroup per row; a given amax (one for
-// the whole matrix) replaces the row's own.
+// E4M3 quantization: amax = max |x| over a row (or the matrix), codes = E4M3(x * (448 /
+// amax)) rounded to nearest even by the conversion instruction, scale = amax / 448 (fp32
+// throughout; an all-zero row gives codes 0 and scale 0).  Rows are read four elements
+// per load (8 bytes of bf16 or 16 bytes of fp32; cols is a multiple of 4).
+struct Quad {
+  float v[4];
+};
 template <class T>
-__device__ __forceinline__ float ldx(const T* p, int64_t i);
+__device__ __forceinline__ Quad ld4(const T* p);
 template <>
-__device__ __forceinline__ float ldx<u16>(const u16* p, int64_t i) { return bf2f(p[i]); }
+__device__ __forceinline__ Quad ld4<u16>(const u16* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return Quad{{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+               __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)}};
+}
 template <>
-__device__ __forceinline__ float ldx<float>(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ Quad ld4<float>(const float* p) {
+  const float4 f = *reinterpret_cast<const float4*>(p);
+  return Quad{{f.x, f.y, f.z, f.w}};
+}
 
 __device__ __forceinline__ float block_max_256(float v, float* red) {
 #pragma unroll
@@ -566,44 +576,72 @@ __device__ __forceinline__ float block_max_256(float v, float* red) {
 }
 
 template <class T>
-__global__ __launch_bounds__(256) void row_amax_kernel(const T* __restrict__ x, int cols,
-                                                       float* __restrict__ amax) {
-  __shared__ float red[4];
-  const T* row = x + int64_t(blockIdx.x) * cols;
+__device__ __forceinline__ float row_amax(const T* row, int cols, float* red) {
   float m = 0.f;
-  for (int c = threadIdx.x; c < cols; c += 256) m = fmaxf(m, fabsf(ldx<T>(row, c)));
-  m = block_max_256(m, red);
-  if (threadIdx.x == 0) amax[blockIdx.x] = m;
-}
-
-// max over n values into out[0] (one workgroup)
-__global__ __launch_bounds__(256) void max_reduce_kernel(const float* __restrict__ v, int64_t n,
-                                                         float* __restrict__ out) {
-  __shared__ float red[4];
-  float m = 0.f;
-  for (int64_t i = threadIdx.x; i < n; i += 256) m = fmaxf(m, v[i]);
-  m = block_max_256(m, red);
-  if (threadIdx.x == 0) out[0] = m;
+  for (int c = threadIdx.x * 4; c < cols; c += 1024) {
+    const Quad q = ld4<T>(row + c);
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(q.v[0]), fabsf(q.v[1])), fmaxf(fabsf(q.v[2]), fabsf(q.v[3]))));
+  }
+  return block_max_256(m, red);
 }
 
 template <class T>
-__global__ __launch_bounds__(256) void quantize_e4m3_kernel(const T* __restrict__ x, int cols,
-                                                            const float* __restrict__ amax_in,
-                                                            int per_row, uint8_t* __restrict__ q,
-                                                            float* __restrict__ scale) {
-  const int64_t r = blockIdx.x;
-  const float amax = amax_in[per_row ? r : 0];
+__device__ __forceinline__ void quantize_row(const T* row, int cols, float amax, uint8_t* q) {
   const float inv = amax > 0.f ? 448.f / amax : 0.f;
-  if (threadIdx.x == 0 && (per_row || r == 0)) scale[per_row ? r : 0] = amax / 448.f;
-  const T* row = x + r * cols;
-  uint32_t* out = reinterpret_cast<uint32_t*>(q + r * cols);
+  uint32_t* out = reinterpret_cast<uint32_t*>(q);
   for (int c = threadIdx.x * 4; c < cols; c += 1024) {
-    const float a = ldx<T>(row, c) * inv, b = ldx<T>(row, c + 1) * inv;
-    const float d = ldx<T>(row, c + 2) * inv, e = ldx<T>(row, c + 3) * inv;
-    int v = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
-    v = __builtin_amdgcn_cvt_pk_fp8_f32(d, e, v, true);
+    const Quad x = ld4<T>(row + c);
+    int v = __builtin_amdgcn_cvt_pk_fp8_f32(x.v[0] * inv, x.v[1] * inv, 0, false);
+    v = __builtin_amdgcn_cvt_pk_fp8_f32(x.v[2] * inv, x.v[3] * inv, v, true);
     out[c >> 2] = uint32_t(v);
   }
+}
+
+// one scale per row: a workgroup per row reads it twice (the second pass hits the cache)
+template <class T>
+__global__ __launch_bounds__(256) void quantize_rows_kernel(const T* __restrict__ x, int cols,
+                                                            uint8_t* __restrict__ q,
+                                                            float* __restrict__ scale) {
+  __shared__ float red[4];
+  const int64_t r = blockIdx.x;
+  const float amax = row_amax<T>(x + r * cols, cols, red);
+  if (threadIdx.x == 0) scale[r] = amax / 448.f;
+  quantize_row<T>(x + r * cols, cols, amax, q + r * cols);
+}
+
+// one scale for the matrix: row maxima, their maximum, then the codes
+template <class T>
+__global__ __launch_bounds__(256) void row_amax_kernel(const T* __restrict__ x, int cols,
+                                                       float* __restrict__ amax) {
+  __shared__ float red[4];
+  const float m = row_amax<T>(x + int64_t(blockIdx.x) * cols, cols, red);
+  if (threadIdx.x == 0) amax[blockIdx.x] = m;
+}
+
+__global__ __launch_bounds__(1024) void max_reduce_kernel(const float* __restrict__ v, int64_t n,
+                                                          float* __restrict__ out) {
+  __shared__ float red[16];
+  float m = 0.f;
+  for (int64_t i = threadIdx.x; i < n; i += 1024) m = fmaxf(m, v[i]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = red[0];
+    for (int w = 1; w < 16; ++w) t = fmaxf(t, red[w]);
+    out[0] = t;
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void quantize_matrix_kernel(const T* __restrict__ x, int cols,
+                                                              const float* __restrict__ amax,
+                                                              uint8_t* __restrict__ q,
+                                                              float* __restrict__ scale) {
+  const int64_t r = blockIdx.x;
+  if (r == 0 && threadIdx.x == 0) scale[0] = amax[0] / 448.f;
+  quantize_row<T>(x + r * cols, cols, amax[0], q + r * cols);
 }
 
 // z[x_n] of the FP8 head: one wave per entry, the decoded codes' dot product times the
@@ -951,23 +989,29 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
 hipError_t launch_quantize_e4m3(int dtype, const void* x, int64_t rows, int cols, int per_row,
                                 uint8_t* q, float* scale, float* amax_ws, hipStream_t s) {
   if (rows == 0 || cols == 0) return hipSuccess;
-  if (dtype == CC_BF16)
+  const bool bf = dtype == CC_BF16;
+  if (per_row) {
+    if (bf)
+      hipLaunchKernelGGL(quantize_rows_kernel<u16>, dim3(rows), dim3(256), 0, s,
+                         static_cast<const u16*>(x), cols, q, scale);
+    else
+      hipLaunchKernelGGL(quantize_rows_kernel<float>, dim3(rows), dim3(256), 0, s,
+                         static_cast<const float*>(x), cols, q, scale);
+    return hipGetLastError();
+  }
+  if (bf)
     hipLaunchKernelGGL(row_amax_kernel<u16>, dim3(rows), dim3(256), 0, s,
                        static_cast<const u16*>(x), cols, amax_ws);
   else
     hipLaunchKernelGGL(row_amax_kernel<float>, dim3(rows), dim3(256), 0, s,
                        static_cast<const float*>(x), cols, amax_ws);
-  const float* am = amax_ws;
-  if (!per_row) {
-    hipLaunchKernelGGL(max_reduce_kernel, dim3(1), dim3(256), 0, s, amax_ws, rows, amax_ws + rows);
-    am = amax_ws + rows;
-  }
-  if (dtype == CC_BF16)
-    hipLaunchKernelGGL(quantize_e4m3_kernel<u16>, dim3(rows), dim3(256), 0, s,
-                       static_cast<const u16*>(x), cols, am, per_row, q, scale);
+  hipLaunchKernelGGL(max_reduce_kernel, dim3(1), dim3(1024), 0, s, amax_ws, rows, amax_ws + rows);
+  if (bf)
+    hipLaunchKernelGGL(quantize_matrix_kernel<u16>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const u16*>(x), cols, amax_ws + rows, q, scale);
   else
-    hipLaunchKernelGGL(quantize_e4m3_kernel<float>, dim3(rows), dim3(256), 0, s,
-                       static_cast<const float*>(x), cols, am, per_row, q, scale);
+    hipLaunchKernelGGL(quantize_matrix_kernel<float>, dim3(rows), dim3(256), 0, s,
+                       static_cast<const float*>(x), cols, amax_ws + rows, q, scale);
   return hipGetLastError();
 }
 
