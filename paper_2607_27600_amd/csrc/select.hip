@@ -48,7 +48,7 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
                                                           int32_t* __restrict__ keep) {
   __shared__ uint32_t hist[256];
   __shared__ int wsum[SWAVES];
-  __shared__ uint32_t sh_digit, sh_rem;
+  __shared__ uint32_t sh_digit, sh_rem, sh_cnt;
   const SelSeg sg = segs[blockIdx.x];
   const float* s = scores + sg.start;
   int32_t* out = keep + sg.out;
@@ -94,6 +94,7 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
           if (acc + c[j] >= rem) {
             sh_digit = uint32_t(255 - 4 * lane - j);
             sh_rem = rem - acc;
+            sh_cnt = c[j];
             break;
           }
           acc += c[j];
@@ -107,6 +108,9 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
     __syncthreads();
   }
   const uint32_t T = prefix;   // the k-th largest key; keep `rem` of the entries equal to T
+  // the last pass's bucket holds exactly the keys equal to T: when all of them are kept,
+  // ties need no ranking
+  const bool all_ties = sh_cnt == rem;
 
   int ties_before = 0, emitted = 0;
   for (int base = 0; base < n; base += SNT) {
@@ -114,9 +118,9 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
     const uint32_t key = i < n ? order_key(s[i]) : 0u;
     const bool eq = i < n && key == T;
     const bool gt = i < n && key > T;
-    int eq_total;
-    const int tie_rank = ties_before + block_scan(eq, wsum, eq_total);
-    const bool take = gt || (eq && uint32_t(tie_rank) < rem);
+    int eq_total = 0, tie_rank = 0;
+    if (!all_ties) tie_rank = ties_before + block_scan(eq, wsum, eq_total);
+    const bool take = gt || (eq && (all_ties || uint32_t(tie_rank) < rem));
     int take_total;
     const int pos = emitted + block_scan(take, wsum, take_total);
     if (take) out[pos] = i;
@@ -170,7 +174,7 @@ __global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restri
   __shared__ uint32_t tot[256];
   __shared__ __attribute__((aligned(16))) uint32_t tab[RWAVES][RPT];
   __shared__ uint32_t red[2][RWAVES];
-  __shared__ uint32_t sh_digit, sh_rem;
+  __shared__ uint32_t sh_digit, sh_rem, sh_cnt;
   const SelSeg sg = segs[blockIdx.x];
   const int n = sg.len, k = sg.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -271,6 +275,7 @@ __global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restri
           if (acc + c[q] >= rem) {
             sh_digit = uint32_t(255 - 4 * lane - q);
             sh_rem = rem - acc;
+            sh_cnt = c[q];
             break;
           }
           acc += c[q];
@@ -283,6 +288,9 @@ __global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restri
     hi = lo;
   }
   const uint32_t T = kmin + prefix;   // the k-th largest key; keep `rem` of the keys equal to T
+  // keys equal to T: the last pass's bucket (all keys when the range is 0).  The count may
+  // include padding copies of kmin, so equality with rem proves every tie is kept.
+  const bool all_ties = B > 0 && sh_cnt == rem;
 
   // ranks in index order: element (j, t) comes after every element of slots < j and after
   // (j, t') for t' < t.  A wave's count per slot is a ballot popcount; lane j of each wave
@@ -310,18 +318,22 @@ __global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restri
   }
   // slots go in groups of four (one wide table read each); the fences keep the compiler
   // from hoisting every group's reads and ballots at once
-  slot_offsets(eq_bits);
+  if (all_ties) {
+    take_bits |= eq_bits;
+  } else {
+    slot_offsets(eq_bits);
 #pragma unroll
-  for (int q = 0; q < RPT / 4; ++q) {
-    const uint4 o = *reinterpret_cast<const uint4*>(&tab[wave][4 * q]);
-    const uint32_t ov[4] = {o.x, o.y, o.z, o.w};
+    for (int q = 0; q < RPT / 4; ++q) {
+      const uint4 o = *reinterpret_cast<const uint4*>(&tab[wave][4 * q]);
+      const uint32_t ov[4] = {o.x, o.y, o.z, o.w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = 4 * q + e;
-      const uint32_t rank = ov[e] + __popcll(__ballot((eq_bits >> j) & 1u) & below);
-      take_bits |= uint32_t(((eq_bits >> j) & 1u) && rank < rem) << j;
+      for (int e = 0; e < 4; ++e) {
+        const int j = 4 * q + e;
+        const uint32_t rank = ov[e] + __popcll(__ballot((eq_bits >> j) & 1u) & below);
+        take_bits |= uint32_t(((eq_bits >> j) & 1u) && rank < rem) << j;
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
   }
   slot_offsets(take_bits);
 #pragma unroll
