@@ -122,3 +122,64 @@ def test_calls_with_bad_arguments_enqueue_nothing():
     assert lib.cc_linear(5, None, None, None, 4, 4, 64, None) == cc.CC_ERR_DTYPE
     for s in range(7):
         assert cc.cc_status_str(s)
+
+
+def test_fused_and_fp8_entry_points_validate_on_the_host():
+    """The W_o-fusion and FP8 entry points reject bad shapes, dtypes and alignments before
+    anything is enqueued, and their workspace queries are host-only."""
+    from paper_2607_27600_amd import cc
+    lib = cc._lib
+    n = ctypes.c_size_t(0)
+    dummy = ctypes.c_void_p(0x1000)     # never dereferenced: every case fails first
+    odd = ctypes.c_void_p(0x1002)
+    # fused weight
+    assert lib.cc_fuse_wo_lmhead_workspace(cc.CC_BF16, 4096, 4096, ctypes.byref(n)) == cc.CC_OK
+    assert n.value >= 4096 * 4096 * 2
+    assert lib.cc_fuse_wo_lmhead_workspace(9, 4096, 4096, ctypes.byref(n)) == cc.CC_ERR_DTYPE
+    assert lib.cc_fuse_wo_lmhead(cc.CC_BF16, dummy, dummy, dummy, 100, 100, 128, dummy, 1 << 30,
+                                 None) == cc.CC_ERR_UNSUPPORTED          # hidden % 64
+    assert lib.cc_fuse_wo_lmhead(cc.CC_BF16, odd, dummy, dummy, 100, 128, 128, dummy, 1 << 30,
+                                 None) == cc.CC_ERR_ARG                  # alignment
+    assert lib.cc_fuse_wo_lmhead(cc.CC_BF16, dummy, dummy, dummy, 100, 128, 128, dummy, 16,
+                                 None) == cc.CC_ERR_WORKSPACE
+    assert lib.cc_fuse_wo_lmhead(cc.CC_BF16, None, dummy, dummy, 100, 128, 128, dummy, 1 << 30,
+                                 None) == cc.CC_ERR_ARG
+    # fused mode: a problem in that mode passes validation; W_o may be null, q may not
+    p, _keep = _prob(mode=cc.CC_MODE_LAST_LAYER_FUSED)
+    assert lib.cc_score_workspace(ctypes.byref(p), ctypes.byref(n)) == cc.CC_OK
+    fused_ws = n.value
+    q2, _k2 = _prob()
+    assert lib.cc_score_workspace(ctypes.byref(q2), ctypes.byref(n)) == cc.CC_OK
+    assert fused_ws < n.value               # no W_o output buffer in the fused layout
+    q3, _k3 = _prob(mode=4)
+    assert lib.cc_score_workspace(ctypes.byref(q3), ctypes.byref(n)) == cc.CC_ERR_ARG
+    # quantization
+    assert lib.cc_quantize_fp8_workspace(1000, ctypes.byref(n)) == cc.CC_OK and n.value >= 4004
+    assert lib.cc_quantize_fp8_workspace(-1, ctypes.byref(n)) == cc.CC_ERR_ARG
+    big = ctypes.c_size_t(1 << 30)
+    assert lib.cc_quantize_fp8(cc.CC_BF16, dummy, 10, 6, 1, dummy, dummy, dummy, big,
+                               None) == cc.CC_ERR_SHAPE                  # cols % 4
+    assert lib.cc_quantize_fp8(cc.CC_BF16, dummy, 10, 8, 2, dummy, dummy, dummy, big,
+                               None) == cc.CC_ERR_ARG                    # per_row flag
+    assert lib.cc_quantize_fp8(cc.CC_F32, odd, 10, 8, 1, dummy, dummy, dummy, big,
+                               None) == cc.CC_ERR_ARG                    # x alignment
+    assert lib.cc_quantize_fp8(cc.CC_F32, dummy, 10, 8, 1, odd, dummy, dummy, big,
+                               None) == cc.CC_ERR_ARG                    # codes alignment
+    assert lib.cc_quantize_fp8(cc.CC_F32, dummy, 10, 8, 1, dummy, dummy, dummy, 8,
+                               None) == cc.CC_ERR_WORKSPACE
+    assert lib.cc_quantize_fp8(3, dummy, 10, 8, 1, dummy, dummy, dummy, big,
+                               None) == cc.CC_ERR_DTYPE
+    assert lib.cc_quantize_fp8(cc.CC_F32, dummy, 0, 8, 1, None, None, None, 0, None) == cc.CC_OK
+    # FP8 LM head
+    p, _keep = _prob()
+    assert lib.cc_lmhead_fp8_workspace(ctypes.byref(p), ctypes.byref(n)) == cc.CC_OK
+    assert n.value >= 250 * 4096 + 501 * 250 * 8
+    q4, _k4 = _prob(hidden=4032)            # a multiple of 64, not of 128
+    assert lib.cc_lmhead_score_fp8(ctypes.byref(q4), dummy, dummy, dummy, dummy, dummy, None,
+                                   dummy, big, None) == cc.CC_ERR_UNSUPPORTED
+    assert lib.cc_lmhead_score_fp8(ctypes.byref(p), dummy, odd, dummy, dummy, dummy, None,
+                                   dummy, big, None) == cc.CC_ERR_ARG    # codes alignment
+    assert lib.cc_lmhead_score_fp8(ctypes.byref(p), dummy, dummy, None, dummy, dummy, None,
+                                   dummy, big, None) == cc.CC_ERR_ARG    # no scale
+    assert lib.cc_lmhead_score_fp8(ctypes.byref(p), dummy, dummy, dummy, dummy, dummy, None,
+                                   dummy, 64, None) == cc.CC_ERR_WORKSPACE
