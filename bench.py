@@ -32,7 +32,9 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    # the LM-head GEMM speeds up over its first ~10 launches after an idle gap (the clock
+    # settles under load)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="C2")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=256)
@@ -184,10 +186,10 @@ def bench_generic(args, cfg, dev) -> dict:
             cc.cc_compact_rows(p, h_rows, keep, ks, per_head, workspace=ws_rows)
         mark(3)
 
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(evs[i])
@@ -495,13 +497,16 @@ def main():
     # the sub-step chain is the same work as cc_score; check once that they agree
     ref_scores = torch.empty_like(scores)
     cc.cc_score(p, w.inputs(), ref_scores)
-    for _ in range(args.warmup):
-        step()
+    step()
     torch.cuda.synchronize()
-    if not torch.equal(ref_scores, scores) and args.warmup > 0:
+    if not torch.equal(ref_scores, scores):
         raise SystemExit("sub-step chain and cc_score disagree")
 
+    # The clock drops in any idle gap and takes about ten LM-head launches to settle again,
+    # so the warm-up runs right before the timed steps with only the synchronisation between.
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
