@@ -26,7 +26,8 @@ from . import cc
 @dataclasses.dataclass
 class Model:
     """Shapes and weights the scoring pass needs (device tensors in bf16)."""
-    mode: str                         # "last_layer" (queries given) or "last_layer_h"
+    mode: str                         # "last_layer" (queries given), "last_layer_fused" (queries
+                                      # given, w_lm = W_lm W_o) or "last_layer_h"
     n_layers: int                     # cache layers
     n_heads_q: int
     n_heads_kv: int
@@ -44,7 +45,7 @@ class Model:
     @property
     def row_width(self) -> int:
         """Elements of the per-entry row the mode scores from (Q or H)."""
-        return self.n_heads_q * self.head_dim if self.mode == "last_layer" else self.hidden
+        return self.hidden if self.mode == "last_layer_h" else self.n_heads_q * self.head_dim
 
 
 class RefreshLoop:
@@ -52,8 +53,8 @@ class RefreshLoop:
 
     def __init__(self, model: Model, J: int, h: int, device="cuda",
                  capacity: Optional[int] = None):
-        if model.mode not in ("last_layer", "last_layer_h"):
-            raise ValueError("mode must be last_layer or last_layer_h")
+        if model.mode not in ("last_layer", "last_layer_fused", "last_layer_h"):
+            raise ValueError("mode must be last_layer, last_layer_fused or last_layer_h")
         if J < 1 or h < 1:
             raise ValueError("J and h must be positive")
         self.m, self.J, self.h = model, J, h
@@ -97,7 +98,7 @@ class RefreshLoop:
 
     def inputs(self) -> cc.Inputs:
         m, n = self.m, self.n
-        if m.mode == "last_layer":
+        if m.mode in ("last_layer", "last_layer_fused"):
             return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=m.w_lm, w_o=m.w_o,
                              q=self.rows[:n])
         return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=m.w_lm, layers=[m.layer],

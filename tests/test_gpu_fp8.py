@@ -81,6 +81,31 @@ def test_lmhead_fp8_matches_quantized_oracle():
     assert d.max() < 0.5
 
 
+def test_lmhead_fp8_from_fp32_rows():
+    """fp32 activations (problem dtype f32) are quantized from their fp32 values."""
+    from paper_2607_27600_amd import cc
+    r = np.random.default_rng(13)
+    N, D, V = 77, 256, 700
+    u = (3 * r.standard_normal((N, D))).astype(np.float32)
+    w = (0.05 * r.standard_normal((V, D))).astype(np.float32)
+    ids = r.integers(0, V, N).astype(np.int32)
+    wc, ws = cc.cc_quantize_fp8("f32", dev(w), per_row=False)
+    p = cc.problem(dtype="f32", cu_seqlens=[0, 40, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
+                   hidden=D, vocab=V)
+    scores = torch.empty(N, dtype=torch.float32, device="cuda")
+    cc.cc_lmhead_score_fp8(p, dev(u), wc, ws, dev(ids), scores)
+    torch.cuda.synchronize()
+    wc_ref, ws_ref = O.quantize_fp8(w, per_row=False)
+    np.testing.assert_array_equal(wc.cpu().numpy(), wc_ref)
+    ref = O.lmhead_fp8_scores(u, wc_ref, ws_ref[0], ids, [0, 40, N])
+    got = scores.cpu().numpy()
+    np.testing.assert_array_equal(np.isinf(got), np.isinf(ref))
+    fin = np.isfinite(ref)
+    err = np.abs(got[fin] - ref[fin])
+    print(f"[fp8 lmhead] f32 rows: max abs {err.max():.3e}", flush=True)
+    assert np.all(err <= FP8_ATOL + FP8_RTOL * np.abs(ref[fin]))
+
+
 def test_lmhead_fp8_zero_head_gives_ln_vocab():
     from paper_2607_27600_amd import cc
     N, D, V = 64, 128, 5000

@@ -4,7 +4,8 @@ At every refresh: the scores equal the oracle's on the cache as it stands (all r
 bf16 tolerance), the keep list equals the oracle's selection on the GPU's own scores,
 and afterwards keys, values, ids, positions and per-entry rows are the byte-exact
 gather.  Across the stream every cached entry keeps the position and id it was
-appended with.  Exact fast variant (from H) and given-query variant; chunked and
+appended with.  Exact fast variant (from H), given-query variant and its form with W_o
+folded into the LM head (scored against the oracle's two-step chain); chunked and
 prefill-end modes."""
 import numpy as np
 import pytest
@@ -37,8 +38,12 @@ def _model(mode):
                            mlp_norm=gen.f32_to_bf16_bits(np.ones(D, np.float32)),
                            w_gate=w(5, (F, D)), w_up=w(6, (F, D)), w_down=w(7, (D, F))),
                 final_norm=gen.f32_to_bf16_bits(np.ones(D, np.float32)))
+    w_lm = dev(host["w_lm"])
+    if mode == "last_layer_fused":      # the GPU model holds W_lm W_o; the oracle the two
+        from paper_2607_27600_amd import cc
+        w_lm = cc.cc_fuse_wo_lmhead("bf16", w_lm, dev(host["w_o"]))
     m = Model(mode=mode, n_layers=L, n_heads_q=HQ, n_heads_kv=HKV, head_dim=D_HEAD, hidden=D,
-              vocab=V, w_lm=dev(host["w_lm"]), w_o=dev(host["w_o"]),
+              vocab=V, w_lm=w_lm, w_o=dev(host["w_o"]),
               layer={k: dev(v) for k, v in host["layer"].items()},
               final_norm=dev(host["final_norm"]), ffn=F, rope_theta=THETA, rms_eps=EPS)
     return m, host
@@ -61,7 +66,7 @@ def _state(loop):
 
 
 @pytest.mark.parametrize("mode,chunked", [("last_layer_h", True), ("last_layer", True),
-                                          ("last_layer_h", False)])
+                                          ("last_layer_h", False), ("last_layer_fused", True)])
 def test_refresh_loop(mode, chunked):
     from paper_2607_27600_amd.refresh import RefreshLoop, run_stream
     print(f"[refresh loop] mode={mode} chunked={chunked}", flush=True)
