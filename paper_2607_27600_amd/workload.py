@@ -122,6 +122,8 @@ class Workload:
                     dst[l].copy_(to_device(pool, "cpu"))
                     if keep_host and l == L - 1:
                         self.host[which] = src
+                    if keep_host and cfg.mode == "full":
+                        self.host.setdefault("kv_layers", {}).setdefault(l, {})[which] = src
             self.kv = cc.kv_paged(self.k_cache, self.v_cache, self.block_table, n_layers=L,
                                   layer_stride=n_pages * hkv * P * d, page_stride=hkv * P * d,
                                   head_stride=P * d, tok_stride=d, page_size=P)

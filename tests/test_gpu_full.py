@@ -44,3 +44,12 @@ def test_full_ragged_batch_gqa_all_rows():
                    vocab=3000, n_heads_q=8, n_heads_kv=2, keep=(10, 1, 50))
     got, ref = _full_case(cfg)
     print(assert_scores_close(got, ref, "bf16", "full-ragged"))
+
+
+def test_full_paged_pool_all_rows():
+    """Every layer's keys/values read from a shuffled paged pool (16-key pages)."""
+    cfg = C.shrink(C.C4, seq_lens=(150, 33, 64), n_layers=2, cache_layers=2, hidden=256, ffn=512,
+                   vocab=1000, n_heads_q=4, n_heads_kv=2, keep=(30, 7, 12), paged=True,
+                   page_size=16)
+    got, ref = _full_case(cfg)
+    print(assert_scores_close(got, ref, "bf16", "full-paged"))

@@ -110,6 +110,26 @@ def test_score_bf16_small_all_rows():
     print(assert_scores_close(got, ref, "bf16", "bf16-small"))
 
 
+def test_score_inclusive_diagonal():
+    """Mask j >= i (each entry also attends to itself); the last entry still scores +inf."""
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.shrink(C.C2, seq_lens=(130, 1, 70), hidden=256, vocab=1000, cache_layers=1,
+                   keep=(30, 1, 10))
+    print(f"[score] inclusive lens={cfg.seq_lens}", flush=True)
+    w = Workload(cfg, cache_layers=1, keep_host=True)
+    p = cc.problem(dtype="bf16", cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=cfg.n_heads_q,
+                   n_heads_kv=cfg.n_heads_kv, head_dim=cfg.head_dim, hidden=cfg.hidden,
+                   vocab=cfg.vocab, diag="inclusive")
+    scores = torch.full((cfg.n_tokens,), float("nan"), dtype=torch.float32, device="cuda")
+    cc.cc_score(p, w.inputs(), scores)
+    torch.cuda.synchronize()
+    h = w.host
+    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                              cfg.cu_seqlens, diag="inclusive")
+    print(assert_scores_close(scores.cpu().numpy(), ref, "bf16", "inclusive"))
+
+
 def test_score_bf16_paged_ragged_all_rows():
     cfg = C.shrink(C.C5, seq_lens=(33, 1, 150, 64), hidden=512, vocab=3000, cache_layers=1,
                    keep=(1, 1, 1, 1))
