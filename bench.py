@@ -161,10 +161,13 @@ def bench_generic(args, cfg, dev) -> dict:
             ks.append(int(cfg.keep[b]))
     scores = torch.empty(N, dtype=torch.float32, device=dev)
     keep = torch.empty(sum(ks), dtype=torch.int32, device=dev)
+    # packed LM head: W_lm packed once per model (outside the timed region)
+    w_packed = cc.cc_pack_lmhead(w.w_lm)
+    p = cc.packed(p)
     ws_score = torch.empty(max(1, cc.cc_score_workspace(p)), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(max(1, cc.cc_select_workspace(len(ks))), dtype=torch.uint8, device=dev)
     ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, per_head)), dtype=torch.uint8, device=dev)
-    inp = w.inputs()
+    inp = w.inputs(w_packed)
     stream = torch.cuda.current_stream()
     h_rows = w.h_last if cfg.mode == "last_layer_h" else None
     ws_rows = None
@@ -220,7 +223,8 @@ def bench_generic(args, cfg, dev) -> dict:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.description}", "n_cached": N, "n_seqs": cfg.n_seqs,
-                   "cache_layers": L, "paged": bool(cfg.paged), "mode": cfg.mode},
+                   "cache_layers": L, "paged": bool(cfg.paged), "mode": cfg.mode,
+                   "lmhead": "packed"},
         "breakdown_ms": part,
         "score_tflops": score_flop / (part["score"] * 1e-3) / 1e12,
         "compact": {"bytes_moved": moved, "ms": part["compact_in_place"],
@@ -311,7 +315,7 @@ def fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len,
     dev = scores.device
     pf = cc.problem(dtype="bf16", cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=Hq,
                     n_heads_kv=cfg.n_heads_kv, head_dim=d, hidden=cfg.hidden, vocab=V,
-                    device=dev, mode="last_layer_fused")
+                    device=dev, mode="last_layer_fused", lmhead_packed=True)
     m = torch.empty((V, Hq * d), dtype=torch.bfloat16, device=dev)
     ws_fuse = torch.empty(cc.cc_fuse_wo_lmhead_workspace("bf16", cfg.hidden, Hq * d),
                           dtype=torch.uint8, device=dev)
@@ -323,7 +327,8 @@ def fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len,
     torch.cuda.synchronize()
     fuse_ms = ev[0].elapsed_time(ev[1])
     del ws_fuse
-    inp = cc.inputs(kv=w.kv, token_ids=w.ids, w_lm=m, q=w.q)
+    m_packed = cc.cc_pack_lmhead(m)
+    inp = cc.inputs(kv=w.kv, token_ids=w.ids, w_lm=m, q=w.q, w_lm_packed=m_packed)
     ws = torch.empty(cc.cc_score_workspace(pf), dtype=torch.uint8, device=dev)
     s_fused = torch.empty_like(scores)
 
@@ -342,12 +347,13 @@ def fused_step_timing(args, cc, w, p, cfg, scores, keep, ks, seg_start, seg_len,
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     fin = torch.isfinite(scores)
     diff = float((s_fused[fin] - scores[fin]).abs().max().item()) if bool(fin.any()) else 0.0
-    del m, ws
+    del m, m_packed, ws
     return {"ms_per_step": ms, "tokens_per_s": N / (ms * 1e-3),
             "speedup_vs_two_step": ms_two_step / ms, "fuse_weight_ms": fuse_ms,
             "max_abs_score_diff_vs_two_step": diff,
-            "note": "W_lm W_o made once per model (fuse_weight_ms, outside the step); step = "
-                    "attention -> LM head on the product -> select -> compaction"}
+            "note": "W_lm W_o made and packed once per model (fuse_weight_ms, outside the "
+                    "step); step = attention -> packed LM head on the product -> select -> "
+                    "compaction"}
 
 
 def fp8_step_timing(args, cc, w, p, cfg, o, u, scores_bf16, ks, seg_start, seg_len, ws_att,
@@ -455,7 +461,17 @@ def main():
     scores = torch.empty(N, dtype=torch.float32, device=dev)
     keep = torch.empty(n_lists * k_keep, dtype=torch.int32, device=dev)
     ws_att = torch.empty(max(1, cc.cc_attention_workspace(p)), dtype=torch.uint8, device=dev)
-    ws_lm = torch.empty(max(1, cc.cc_lmhead_workspace(p)), dtype=torch.uint8, device=dev)
+    # The LM head reads W_lm in the packed layout (cc_pack_lmhead), made once per model like
+    # any weight preparation and timed apart; the entry rows are packed inside every step.
+    pp = cc.packed(p)
+    w_packed = cc.cc_pack_lmhead(w.w_lm)
+    ev_pk = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev_pk[0].record()
+    cc.cc_pack_lmhead(w.w_lm, out=w_packed)
+    ev_pk[1].record()
+    torch.cuda.synchronize()
+    pack_w_ms = ev_pk[0].elapsed_time(ev_pk[1])
+    ws_lm = torch.empty(max(1, cc.cc_lmhead_workspace(pp)), dtype=torch.uint8, device=dev)
     ws_sel = torch.empty(max(1, cc.cc_select_workspace(n_lists)), dtype=torch.uint8, device=dev)
     ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, int(cfg.per_head_select))),
                          dtype=torch.uint8, device=dev)
@@ -479,7 +495,7 @@ def main():
         mark(1)
         cc.cc_linear("bf16", o.view(N, Hq * d), w.w_o, u)
         mark(2)
-        cc.cc_lmhead_score(p, u, w.w_lm, w.ids, scores, workspace=ws_lm)
+        cc.cc_lmhead_score_packed(pp, u, w.w_lm, w_packed, w.ids, scores, workspace=ws_lm)
         mark(3)
         cc.cc_select_keep(scores, seg_start, seg_len, ks, keep, ws_sel)
         mark(4)
@@ -496,7 +512,7 @@ def main():
 
     # the sub-step chain is the same work as cc_score; check once that they agree
     ref_scores = torch.empty_like(scores)
-    cc.cc_score(p, w.inputs(), ref_scores)
+    cc.cc_score(pp, w.inputs(w_packed), ref_scores)
     step()
     torch.cuda.synchronize()
     if not torch.equal(ref_scores, scores):
@@ -518,6 +534,22 @@ def main():
         for j, n in enumerate(names):
             part_ms[n] += e[j].elapsed_time(e[j + 1]) / args.steps
     ms_step = elapsed * 1e3 / args.steps
+
+    # the row-major LM head on the same rows, for comparison (same warm-up rule)
+    ws_rm = torch.empty(max(1, cc.cc_lmhead_workspace(p)), dtype=torch.uint8, device=dev)
+    s_rm = torch.empty_like(scores)
+    ev_rm = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(args.warmup):
+        cc.cc_lmhead_score(p, u, w.w_lm, w.ids, s_rm, workspace=ws_rm)
+    ev_rm[0].record(stream)
+    for _ in range(args.steps):
+        cc.cc_lmhead_score(p, u, w.w_lm, w.ids, s_rm, workspace=ws_rm)
+    ev_rm[1].record(stream)
+    torch.cuda.synchronize()
+    rm_ms = ev_rm[0].elapsed_time(ev_rm[1]) / args.steps
+    fin = torch.isfinite(scores)
+    rm_diff = float((s_rm[fin] - scores[fin]).abs().max().item()) if bool(fin.any()) else 0.0
+    del ws_rm, s_rm
 
     # NEXT-4 alternative: W_o folded into the LM head (mode LAST_LAYER_FUSED).  The product
     # weight is made once per model (timed apart, not part of a step); a fused step is
@@ -571,8 +603,9 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.description}", "n_cached": N,
                    "n_heads_q": Hq, "n_heads_kv": hkv, "head_dim": d, "hidden": D, "vocab": V,
                    "keep": k_keep, "cache_layers": L, "variant": "fast last-layer"},
-        "roofline": {"kernel": "LM head GEMM + fused log-sum-exp (gemm_tn_bf16<EpiLse> + "
-                               "lse_combine)",
+        "roofline": {"kernel": "LM head GEMM on packed operands + fused log-sum-exp "
+                               "(pack_rows of U + gemm_lmhead_packed<EpiLse16> + target_logit "
+                               "+ lse_combine)",
                      "bound": "mfma", "achieved": lm_tflops, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": lm_tflops / PEAK_BF16_TFLOPS, "traffic": lmhead_traffic(),
                      "flop_per_launch": lm_flop},
@@ -586,6 +619,12 @@ def main():
                              "gb_s_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9,
                              "frac_hbm_cache_flushed": 2 * kept_bytes / (ip_flushed * 1e-3) / 1e9 / PEAK_HBM_GBS},
         "select_sweep": sweep,
+        "lmhead_layout": {"packed": True, "pack_w_lm_ms": pack_w_ms,
+                          "row_major_lmhead_ms": rm_ms,
+                          "row_major_lmhead_tflops": lm_flop / (rm_ms * 1e-3) / 1e12,
+                          "max_abs_score_diff_row_major": rm_diff,
+                          "note": "W_lm packed once per model (pack_w_lm_ms, outside the step); "
+                                  "the row-major kernel on the same rows for comparison"},
         "fused_wo_lmhead": fused,
         "lmhead_fp8": fp8,
         "breakdown_ms": part_ms,

@@ -129,6 +129,9 @@ typedef struct cc_problem {
   float rms_eps;               /* FULL, LAST_LAYER_H: RMSNorm epsilon */
   int32_t n_frozen;            /* first n_frozen entries of each sequence are sink
                                   slots that are never evicted (score +inf) */
+  int32_t lmhead_packed;       /* bf16 only: 1 = the LM head reads the packed weight
+                                  cc_inputs.w_lm_packed (cc_pack_lmhead) and packs its
+                                  input rows in the workspace; 0 = row-major w_lm only */
 } cc_problem;
 
 /* Weights of one transformer layer (FULL, LAST_LAYER_H), device pointers in `dtype`. */
@@ -159,6 +162,9 @@ typedef struct cc_inputs {
   const void* final_norm;      /* FULL, LAST_LAYER_H: [D] final RMSNorm gain */
   const void* h_last;          /* LAST_LAYER_H: [N][D] stored activations entering
                                   the last layer (dtype), token-major like ids */
+  const void* w_lm_packed;     /* lmhead_packed = 1: w_lm in the packed layout of
+                                  cc_pack_lmhead (w_lm is still read for the target
+                                  logits) */
 } cc_inputs;
 
 /* Human-readable name of a status code (static string). */
@@ -249,6 +255,30 @@ cc_status cc_lmhead_score_fp8(const cc_problem* p, const void* u, const uint8_t*
                               const float* w_scale, const int32_t* token_ids, float* scores,
                               float* lse, void* workspace, size_t workspace_bytes,
                               void* stream);
+
+/* Bytes of the packed LM-head layout of a bf16 [rows][cols] matrix: rows rounded up
+ * to a multiple of 256, times cols, times 2. */
+cc_status cc_pack_lmhead_bytes(int64_t rows, int32_t cols, size_t* bytes);
+
+/* Packs a bf16 matrix x [rows][cols] (row stride cols; cols a positive multiple of 32;
+ * x 16-byte aligned) into the layout the packed LM head stages: for each 256-row tile
+ * and 32-column step, one 16 KB block in which row r (64 bytes at 64r) holds its
+ * 16-byte chunk c (columns 8c .. 8c+7 of the step) at chunk position c ^ ((r >> 2) & 3);
+ * rows past `rows` are zero.  A bit copy that changes the layout only: the weight
+ * preparation for lmhead_packed = 1, made once per model (the LM-head input rows are
+ * packed inside each call).  out: device, cc_pack_lmhead_bytes bytes, 16-byte aligned,
+ * not overlapping x. */
+cc_status cc_pack_lmhead(const void* x, int64_t rows, int32_t cols, void* out,
+                         size_t out_bytes, void* stream);
+
+/* cc_lmhead_score with p->lmhead_packed = 1: w_packed is w_lm [V][D] packed by
+ * cc_pack_lmhead; w_lm itself is read for the target logits only.  The result equals
+ * cc_lmhead_score up to fp32 summation order (the packed kernel accumulates in another
+ * order on the 16x16x32 matrix-core shape).  Workspace: cc_lmhead_workspace(p). */
+cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_lm,
+                                 const void* w_packed, const int32_t* token_ids,
+                                 float* scores, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ selection */
 

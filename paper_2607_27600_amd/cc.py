@@ -30,7 +30,8 @@ EXPORTED = [
     "cc_select_workspace", "cc_select_keep", "cc_compact_workspace", "cc_compact_kv",
     "cc_compact_rows_workspace", "cc_compact_rows", "cc_fuse_wo_lmhead_workspace",
     "cc_fuse_wo_lmhead", "cc_quantize_fp8_workspace", "cc_quantize_fp8",
-    "cc_lmhead_fp8_workspace", "cc_lmhead_score_fp8",
+    "cc_lmhead_fp8_workspace", "cc_lmhead_score_fp8", "cc_pack_lmhead_bytes", "cc_pack_lmhead",
+    "cc_lmhead_score_packed",
 ]
 
 _c_void_p = ctypes.c_void_p
@@ -51,7 +52,7 @@ class c_problem(ctypes.Structure):
                 ("n_heads_q", _i32), ("n_heads_kv", _i32), ("head_dim", _i32),
                 ("hidden", _i32), ("vocab", _i32), ("n_layers", _i32), ("ffn", _i32),
                 ("softmax_scale", ctypes.c_float), ("rope_theta", ctypes.c_float),
-                ("rms_eps", ctypes.c_float), ("n_frozen", _i32)]
+                ("rms_eps", ctypes.c_float), ("n_frozen", _i32), ("lmhead_packed", _i32)]
 
 
 class c_layer_weights(ctypes.Structure):
@@ -64,7 +65,7 @@ class c_inputs(ctypes.Structure):
     _fields_ = [("q", _c_void_p), ("kv", c_kv), ("token_ids", _c_void_p), ("pos_ids", _c_void_p),
                 ("w_o", _c_void_p), ("w_lm", _c_void_p), ("embed", _c_void_p),
                 ("layers_h", ctypes.POINTER(c_layer_weights)), ("final_norm", _c_void_p),
-                ("h_last", _c_void_p)]
+                ("h_last", _c_void_p), ("w_lm_packed", _c_void_p)]
 
 
 def _load():
@@ -95,6 +96,11 @@ def _load():
         "cc_lmhead_score_fp8": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                      _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
                                      _c_void_p]),
+        "cc_pack_lmhead_bytes": (st, [_i64, _i32, sz]),
+        "cc_pack_lmhead": (st, [_c_void_p, _i64, _i32, _c_void_p, ctypes.c_size_t, _c_void_p]),
+        "cc_lmhead_score_packed": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                        _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
+                                        _c_void_p]),
         "cc_fuse_wo_lmhead": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32,
                                    _c_void_p, ctypes.c_size_t, _c_void_p]),
         "cc_select_workspace": (st, [_i32, sz]),
@@ -168,7 +174,8 @@ class Problem:
 def problem(*, dtype: str, cu_seqlens: Sequence[int], n_heads_q: int, n_heads_kv: int,
             head_dim: int, hidden: int, vocab: int, device="cuda", mode: str = "last_layer",
             diag: str = "strict", n_layers: int = 0, ffn: int = 0, softmax_scale: float = 0.0,
-            rope_theta: float = 0.0, rms_eps: float = 0.0, n_frozen: int = 0) -> Problem:
+            rope_theta: float = 0.0, rms_eps: float = 0.0, n_frozen: int = 0,
+            lmhead_packed: bool = False) -> Problem:
     cu_h = torch.as_tensor(list(cu_seqlens), dtype=torch.int32).contiguous()
     cu_d = cu_h.to(device)
     s = c_problem()
@@ -184,7 +191,15 @@ def problem(*, dtype: str, cu_seqlens: Sequence[int], n_heads_q: int, n_heads_kv
     s.hidden, s.vocab, s.n_layers, s.ffn = hidden, vocab, n_layers, ffn
     s.softmax_scale, s.rope_theta, s.rms_eps = softmax_scale, rope_theta, rms_eps
     s.n_frozen = n_frozen
+    s.lmhead_packed = int(lmhead_packed)
     return Problem(s, cu_h, cu_d, torch.device(device))
+
+
+def packed(p: Problem, on: bool = True) -> Problem:
+    """The same problem with the packed LM head switched on (or off)."""
+    s = c_problem.from_buffer_copy(p.struct)
+    s.lmhead_packed = int(on)
+    return Problem(s, p.cu_h, p.cu_d, p.device)
 
 
 @dataclass
@@ -230,7 +245,8 @@ def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[t
            w_o: Optional[torch.Tensor] = None, pos_ids: Optional[torch.Tensor] = None,
            embed: Optional[torch.Tensor] = None, layers: Optional[list] = None,
            final_norm: Optional[torch.Tensor] = None,
-           h_last: Optional[torch.Tensor] = None) -> Inputs:
+           h_last: Optional[torch.Tensor] = None,
+           w_lm_packed: Optional[torch.Tensor] = None) -> Inputs:
     s = c_inputs()
     s.q = q.data_ptr() if q is not None else None
     s.kv = kv.struct
@@ -240,7 +256,8 @@ def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[t
     s.w_lm = w_lm.data_ptr()
     s.embed = embed.data_ptr() if embed is not None else None
     s.h_last = h_last.data_ptr() if h_last is not None else None
-    keep = [kv, token_ids, w_lm, q, w_o, pos_ids, embed, final_norm, h_last]
+    s.w_lm_packed = w_lm_packed.data_ptr() if w_lm_packed is not None else None
+    keep = [kv, token_ids, w_lm, q, w_o, pos_ids, embed, final_norm, h_last, w_lm_packed]
     if layers:
         arr = (c_layer_weights * len(layers))()
         for i, L in enumerate(layers):
@@ -300,6 +317,33 @@ def cc_lmhead_score(p: Problem, u: torch.Tensor, w_lm: torch.Tensor, token_ids: 
     _check(_lib.cc_lmhead_score(ctypes.byref(p.struct), _ptr(u), _ptr(w_lm), _ptr(token_ids),
                                 _ptr(scores), _ptr(lse), _ptr(workspace), workspace.numel(),
                                 _stream(stream)), "cc_lmhead_score")
+    return scores
+
+
+def cc_pack_lmhead_bytes(rows: int, cols: int) -> int:
+    return _query(_lib.cc_pack_lmhead_bytes, rows, cols)
+
+
+def cc_pack_lmhead(x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The packed LM-head layout of a bf16 [rows][cols] matrix (uint8 buffer)."""
+    rows, cols = x.shape
+    need = cc_pack_lmhead_bytes(rows, cols)
+    if out is None:
+        out = torch.empty(need, dtype=torch.uint8, device=x.device)
+    _check(_lib.cc_pack_lmhead(_ptr(x), rows, cols, _ptr(out), out.numel() * out.element_size(),
+                               _stream(stream)), "cc_pack_lmhead")
+    return out
+
+
+def cc_lmhead_score_packed(p: Problem, u: torch.Tensor, w_lm: torch.Tensor, w_packed: torch.Tensor,
+                           token_ids: torch.Tensor, scores: torch.Tensor,
+                           lse: Optional[torch.Tensor] = None, workspace=None, stream=None):
+    if workspace is None:
+        workspace = _workspace(cc_lmhead_workspace(p), p.device)
+    _check(_lib.cc_lmhead_score_packed(ctypes.byref(p.struct), _ptr(u), _ptr(w_lm), _ptr(w_packed),
+                                       _ptr(token_ids), _ptr(scores), _ptr(lse), _ptr(workspace),
+                                       workspace.numel(), _stream(stream)),
+           "cc_lmhead_score_packed")
     return scores
 
 

@@ -58,6 +58,8 @@ cc_status check_problem(const cc_problem* p) {
     if (p->ffn % 64 != 0) return CC_ERR_UNSUPPORTED;
     if (!(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return CC_ERR_ARG;
   }
+  if (p->lmhead_packed != 0 && p->lmhead_packed != 1) return CC_ERR_ARG;
+  if (p->lmhead_packed && p->dtype != CC_BF16) return CC_ERR_UNSUPPORTED;
   return CC_OK;
 }
 
@@ -150,11 +152,20 @@ size_t attention_ws_bytes(const cc_problem* p) {
   return align_up(items * sizeof(int4));
 }
 
+// Input width of the LM head: the model width, or Hq*d for the W_o-folded weight.
+int lmhead_k(const cc_problem* p) {
+  return p->mode == CC_MODE_LAST_LAYER_FUSED ? p->n_heads_q * p->head_dim : p->hidden;
+}
+
+// LM-head workspace: per-(vocabulary tile, entry) partials, target logits and, for the
+// packed LM head, the packed input rows.
 size_t lmhead_ws_bytes(const cc_problem* p) {
   const size_t N = n_tokens(p);
   const int vt = lmhead_vocab_tile(p->dtype);
   const size_t n_vt = (p->vocab + vt - 1) / vt;
-  return align_up(n_vt * N * sizeof(float2)) + align_up(N * sizeof(float));
+  size_t b = align_up(n_vt * N * sizeof(float2)) + align_up(N * sizeof(float));
+  if (p->lmhead_packed) b += align_up(packed_rows_bytes(int64_t(N), lmhead_k(p)));
+  return b;
 }
 
 struct ScoreLayout {
@@ -239,7 +250,8 @@ cc_status run_attention(const cc_problem* p, const void* q, const cc_kv* kv, int
 // LM head over rows u [N][D]; D is the model width unless given (the fused weight's
 // input width Hq*d).
 cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const int32_t* ids,
-                     float* scores, float* lse, void* ws, hipStream_t s, int D = 0) {
+                     float* scores, float* lse, void* ws, hipStream_t s, int D = 0,
+                     const void* w_packed = nullptr) {
   const int N = n_tokens(p);
   const int vt = lmhead_vocab_tile(p->dtype);
   const size_t n_vt = (p->vocab + vt - 1) / vt;
@@ -258,7 +270,19 @@ cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const
   a.D = D > 0 ? D : p->hidden;
   a.V = p->vocab;
   a.n_frozen = p->n_frozen;
+  if (p->lmhead_packed) {
+    if (!w_packed) return CC_ERR_ARG;
+    a.w_packed = w_packed;
+    a.u_packed = at(ws, align_up(n_vt * N * sizeof(float2)) + align_up(N * sizeof(float)));
+  }
   CC_HIP(launch_lmhead(a, s));
+  return CC_OK;
+}
+
+// The packed LM head needs its weight (checked before anything is launched).
+cc_status check_packed(const cc_problem* p, const void* w_packed) {
+  if (!p->lmhead_packed || n_tokens(p) == 0) return CC_OK;
+  if (!w_packed || !aligned16(w_packed)) return CC_ERR_ARG;
   return CC_OK;
 }
 
@@ -289,6 +313,7 @@ cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, vo
         if (!q || !aligned16(q)) return CC_ERR_ARG;
     }
   }
+  CC_TRY(check_packed(p, in->w_lm_packed));
   const FullLayout L = full_layout(p);
   CC_TRY(check_ws(ws, ws_bytes, L.total));
   if (N == 0) return CC_OK;
@@ -314,7 +339,8 @@ cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, vo
     CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
   }
   CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
-  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, 0,
+                    in->w_lm_packed);
 }
 
 // The exact fast variant (Sec. 3.1, fast single-layer approximation): one layer of the
@@ -335,6 +361,7 @@ cc_status score_last_h(const cc_problem* p, const cc_inputs* in, float* scores, 
     for (const void* q : ptrs)
       if (!q || !aligned16(q)) return CC_ERR_ARG;
   }
+  CC_TRY(check_packed(p, in->w_lm_packed));
   const FullLayout L = full_layout(p);
   CC_TRY(check_ws(ws, ws_bytes, L.total));
   if (N == 0) return CC_OK;
@@ -358,7 +385,8 @@ cc_status score_last_h(const cc_problem* p, const cc_inputs* in, float* scores, 
   CC_HIP(launch_gate_up_swiglu(W.w_gate, W.w_up, a, act, N, D, F, s));
   CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
   CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
-  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+  return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, 0,
+                    in->w_lm_packed);
 }
 
 }  // namespace
@@ -411,8 +439,43 @@ cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
   CC_TRY(check_problem(p));
   if (n_tokens(p) > 0 && (!u || !w_lm || !token_ids || !scores)) return CC_ERR_ARG;
   if (p->dtype == CC_BF16 && (!aligned16(u) || !aligned16(w_lm))) return CC_ERR_ARG;
+  if (p->lmhead_packed && n_tokens(p) > 0) return CC_ERR_ARG;   // cc_lmhead_score_packed
   CC_TRY(check_ws(ws, ws_bytes, lmhead_ws_bytes(p)));
   return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream));
+}
+
+cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_lm,
+                                 const void* w_packed, const int32_t* token_ids,
+                                 float* scores, float* lse, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  CC_TRY(check_problem(p));
+  if (!p->lmhead_packed) return CC_ERR_ARG;
+  if (n_tokens(p) > 0 && (!u || !w_lm || !token_ids || !scores)) return CC_ERR_ARG;
+  if (!aligned16(u) || !aligned16(w_lm)) return CC_ERR_ARG;
+  CC_TRY(check_packed(p, w_packed));
+  CC_TRY(check_ws(ws, ws_bytes, lmhead_ws_bytes(p)));
+  return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream), 0,
+                    w_packed);
+}
+
+cc_status cc_pack_lmhead_bytes(int64_t rows, int32_t cols, size_t* bytes) {
+  if (!bytes || rows < 0 || cols < 1 || cols % 32 != 0) return CC_ERR_ARG;
+  *bytes = packed_rows_bytes(rows, cols);
+  return CC_OK;
+}
+
+cc_status cc_pack_lmhead(const void* x, int64_t rows, int32_t cols, void* out,
+                         size_t out_bytes, void* stream) {
+  size_t need = 0;
+  CC_TRY(cc_pack_lmhead_bytes(rows, cols, &need));
+  if (rows == 0) return CC_OK;
+  if (!x || !out || !aligned16(x) || !aligned16(out)) return CC_ERR_ARG;
+  if (out_bytes < need) return CC_ERR_WORKSPACE;
+  const char* xb = static_cast<const char*>(x);
+  const char* ob = static_cast<const char*>(out);
+  if (ob < xb + size_t(rows) * cols * 2 && xb < ob + need) return CC_ERR_ARG;   // overlap
+  CC_HIP(launch_pack_rows(x, rows, cols, cols, out, static_cast<hipStream_t>(stream)));
+  return CC_OK;
 }
 
 cc_status cc_linear(int32_t dtype, const void* x, const void* w, void* y, int32_t M, int32_t N,
@@ -450,6 +513,7 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   if (p->dtype == CC_BF16 &&
       (!aligned16(in->q) || (!fused && !aligned16(in->w_o)) || !aligned16(in->w_lm)))
     return CC_ERR_ARG;
+  CC_TRY(check_packed(p, in->w_lm_packed));
   const ScoreLayout L = score_layout(p);
   CC_TRY(check_ws(ws, ws_bytes, L.total));
   if (N == 0) return CC_OK;
@@ -459,9 +523,11 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   CC_TRY(run_attention(p, in->q, &in->kv, in->kv.n_layers - 1, o, at(ws, L.attn), s));
   const int qdim = p->n_heads_q * p->head_dim;
   if (fused)   // z = (W_lm W_o) y straight from the attention rows
-    return run_lmhead(p, o, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, qdim);
+    return run_lmhead(p, o, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, qdim,
+                      in->w_lm_packed);
   CC_HIP(launch_linear(p->dtype, o, in->w_o, u, N, p->hidden, qdim, s));
-  return run_lmhead(p, u, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s);
+  return run_lmhead(p, u, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, 0,
+                    in->w_lm_packed);
 }
 
 // ------------------------------------------------------------------ fused LM-head weight

@@ -109,8 +109,17 @@ struct LmHeadLaunch {
   int n_seqs;
   int N, D, V;
   int n_frozen;
+  // bf16 only, optional: the weight packed by launch_pack_rows; u is then packed into
+  // u_packed (packed_rows_bytes(N, D)) and the packed kernel runs
+  const void* w_packed = nullptr;
+  void* u_packed = nullptr;
 };
 int lmhead_vocab_tile(int dtype);
+// Packed operand layout of the LM head (bf16 [rows][cols], cols a multiple of 32): per
+// 256-row tile and 32-column step a 16 KB block, the LDS image the kernel stages.
+size_t packed_rows_bytes(int64_t rows, int cols);
+hipError_t launch_pack_rows(const void* x, int64_t rows, int cols, int64_t ldx, void* out,
+                            hipStream_t s);
 hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s);
 
 // FP8 LM head: u (dtype) quantized per row into uq / su, then the E4M3 GEMM with the LSE

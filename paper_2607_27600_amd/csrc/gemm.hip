@@ -15,6 +15,8 @@
 // in-lane.  Tiles are rasterised entry-tile-fastest so consecutive workgroups share one
 // LM-head tile.
 // fp32 kernel: a plain LDS-tiled FMA GEMM with the same two epilogues.
+#include <type_traits>
+
 #include "cc_internal.h"
 
 namespace cc {
@@ -428,6 +430,244 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   epi(acc, g, tm, m0 + wm * GTM, n0 + wn * GTN, lane, lds0);
+}
+
+// ------------------------------------------------------------------ packed LM head
+// The same contraction with both operands stored as the LDS images the kernel stages.  A
+// [R][K] matrix is packed per 256-row tile and 32-wide k-step into one 16 KB block: row r of
+// the tile at bytes 64r .. 64r+63, its 16-byte chunk c (k = 8c .. 8c+7 of the step) at
+// chunk position c ^ ((r >> 2) & 3); rows past R are zero.  Staging a block is then a
+// contiguous 16 KB copy (one 1 KB run per wave instruction), which the memory system
+// delivers markedly faster than 256 row pieces of 64 bytes; the XOR spreads the fragment
+// reads of 16 consecutive rows at one chunk over all 64 banks.  The vocabulary weight is
+// packed once per model, the entry rows at every call.
+//
+// Matrix cores: 16x16x32 bf16 MFMA (lane l reads row l%16 of a 16-row block at chunk l/16;
+// it holds rows 4(l/16) .. +3 of column l%16 of the result), 8 waves of 128x64 as 8x4
+// blocks.  Four stages of one k-step each: the loads of k-step t+3 are issued while k-step
+// t is multiplied, so a load has three k-steps to land.
+constexpr int PK_ROWS = 256, PK_K = 32;
+constexpr int PK_BLOCK = PK_ROWS * PK_K;          // elements per packed block (16 KB)
+constexpr int PSTAGE = 2 * PK_BLOCK;              // an A block and a B block (32 KB)
+constexpr int PNST = 4;                           // stages
+constexpr int HMB = GTM / 16, HNB = GTN / 16;     // 8 x 4 MFMA blocks per wave
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// One thread per 16-byte chunk; consecutive threads walk a row (reads of whole rows),
+// each group of four writes the 64 bytes of one packed row.
+__global__ __launch_bounds__(256) void pack_rows_kernel(const u16* __restrict__ x, int R,
+                                                        int K, int64_t ldx, int64_t n_chunks,
+                                                        u16* __restrict__ out) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n_chunks) return;
+  const int nsteps = K / PK_K;
+  const int c = int(i & 3);
+  const int64_t rs = i >> 2;
+  const int s = int(rs % nsteps);
+  const int64_t row = rs / nsteps;
+  const int r = int(row % PK_ROWS);
+  const int64_t t = row / PK_ROWS;
+  const uint4 v = row < R ? ld16(x + row * ldx + s * PK_K + c * 8) : make_uint4(0, 0, 0, 0);
+  u16* dst = out + (t * nsteps + s) * PK_BLOCK + r * PK_K + ((c ^ ((r >> 2) & 3)) * 8);
+  *reinterpret_cast<uint4*>(dst) = v;
+}
+
+// LSE epilogue in the 16x16 layout: each lane holds 32 logits of each of four entries; the
+// four lane groups of an entry combine by shuffles, the two wave rows through LDS.
+struct EpiLse16 {
+  float2* partial;
+  __device__ void operator()(const f32x4 (&acc)[HMB][HNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    const int grp = lane >> 4, c16 = lane & 15;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / WGN, wn = wave % WGN;
+    float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
+    const bool edge = tm * GBM + GBM > g.M;
+    float mx[HNB], sm[HNB], mc[HNB];
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) mx[nb] = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < HMB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = !edge || (m0w + mb * 16 + 4 * grp + e < g.M);
+#pragma unroll
+        for (int nb = 0; nb < HNB; ++nb)
+          if (ok) mx[nb] = fmaxf(mx[nb], acc[mb][nb][e]);
+      }
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) {
+      mc[nb] = mx[nb] == -INFINITY ? 0.f : mx[nb] * kLog2e;
+      sm[nb] = 0.f;
+    }
+#pragma unroll
+    for (int mb = 0; mb < HMB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = !edge || (m0w + mb * 16 + 4 * grp + e < g.M);
+#pragma unroll
+        for (int nb = 0; nb < HNB; ++nb)
+          if (ok) sm[nb] += fast_exp2(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
+      }
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) {
+#pragma unroll
+      for (int off = 16; off < 64; off <<= 1) {
+        const float mx2 = __shfl_xor(mx[nb], off);
+        const float sm2 = __shfl_xor(sm[nb], off);
+        const float M = fmaxf(mx[nb], mx2);
+        float S = 0.f;
+        if (M != -INFINITY)
+          S = sm[nb] * exp2f((mx[nb] - M) * kLog2e) + sm2 * exp2f((mx2 - M) * kLog2e);
+        mx[nb] = M;
+        sm[nb] = S;
+      }
+      if (grp == 0) red[wm * GBN + wn * GTN + nb * 16 + c16] = make_float2(mx[nb], sm[nb]);
+    }
+    __syncthreads();
+    if (wm == 0 && grp == 0) {
+#pragma unroll
+      for (int nb = 0; nb < HNB; ++nb) {
+        const int c = wn * GTN + nb * 16 + c16;
+        const int n = n0w + nb * 16 + c16;
+        float M = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < WGM; ++r) M = fmaxf(M, red[r * GBN + c].x);
+        float S = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll
+          for (int r = 0; r < WGM; ++r) {
+            const float2 p = red[r * GBN + c];
+            S += p.y * exp2f((p.x - M) * kLog2e);
+          }
+        }
+        if (n < g.N) partial[int64_t(tm) * g.N + n] = make_float2(M, S);
+      }
+    }
+  }
+};
+
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+  return reinterpret_cast<const char*>((uint64_t(hi) << 32) | lo);
+}
+
+template <int P>
+using IC = std::integral_constant<int, P>;
+
+// g.A, g.B: packed operands (M and N rows, K a multiple of 32).  Waves 0-3 stage the A block
+// of a k-step, waves 4-7 the B block.  The loads are issued from inline assembly so that the
+// compiler, which cannot tell the four stages apart across the loop, does not order every
+// LDS read after every pending load; their completion is awaited explicitly (vmcnt) before
+// the barrier that precedes the reads of each stage.
+template <class Epi>
+__global__ __launch_bounds__(GNT, 1) void gemm_lmhead_packed(GemmArgs g, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) u16 s0[PSTAGE];
+  __shared__ __attribute__((aligned(1024))) u16 s1[PSTAGE];
+  __shared__ __attribute__((aligned(1024))) u16 s2[PSTAGE];
+  __shared__ __attribute__((aligned(1024))) u16 s3[PSTAGE];
+  auto stg = [&](auto p) -> u16* {
+    constexpr int q = decltype(p)::value % PNST;
+    if constexpr (q == 0) return s0;
+    else if constexpr (q == 1) return s1;
+    else if constexpr (q == 2) return s2;
+    else return s3;
+  };
+  int tm, tn;
+  tile_of(blockIdx.x, g.tiles_m, g.tiles_n, tm, tn);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int grp = lane >> 4, r16 = lane & 15;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int nsteps = g.K / PK_K;
+  const bool isA = wave_u < 4;
+  const char* gbase = isA ? reinterpret_cast<const char*>(g.A + int64_t(tm) * nsteps * PK_BLOCK)
+                          : reinterpret_cast<const char*>(g.B + int64_t(tn) * nsteps * PK_BLOCK);
+  const uint32_t lds_w = uint32_t(wave_u * 4 * 1024);   // this wave's 4 KB of a stage
+  const uint32_t goff = uint32_t(((wave_u & 3) * 4 * 64 + lane) * 16);
+  // instruction j of a step: the wave's j-th 1 KB run of the block (global and LDS)
+  auto dma = [&](u16* stage, int step, int j) {
+    const uint64_t base = reinterpret_cast<uint64_t>(
+        uniform_ptr(gbase + int64_t(min(step, nsteps - 1)) * (PK_BLOCK * 2) + j * 1024));
+    const uint32_t lds = uint32_t(reinterpret_cast<uintptr_t>(stage)) + lds_w + uint32_t(j * 1024);
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(lds), "v"(goff), "s"(base) : "memory", "m0");
+  };
+  // fragment reads: one lane offset (row r16 of a block, chunk grp swizzled by r16 bits 2-3,
+  // the same for every block); the blocks are immediate offsets
+  uint32_t loff = uint32_t(r16 * 64 + ((grp ^ ((r16 >> 2) & 3)) * 16));
+  const uint32_t aoff = uint32_t(wm * GTM * PK_K * 2);
+  const uint32_t boff = uint32_t((GBM + wn * GTN) * PK_K * 2);
+  auto fragA = [&](const u16* S, int mb) {
+    return as_bf16x8(*reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + aoff +
+                                                      loff + mb * 1024));
+  };
+  auto fragB = [&](const u16* S, int nb) {
+    return as_bf16x8(*reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(S) + boff +
+                                                      loff + nb * 1024));
+  };
+  f32x4 acc[HMB][HNB];
+#pragma unroll
+  for (int mb = 0; mb < HMB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) acc[mb][nb] = f32x4{};
+  bf16x8 fa[HMB], fb0[HNB], fb1[HNB];
+  // s_waitcnt vmcnt(4) expcnt(7) lgkmcnt(0): this wave's loads of the next k-step have landed
+  // (the following k-step's four may be in flight) and its fragment reads are complete
+  constexpr int kWaitNext = 4 | (7 << 4);
+  // k-step t (P = t mod 4 fixes the stages and the current B set): MFMAs of k-step t from
+  // registers; fragments of k-step t+1 from its stage (A refilled block by block after the
+  // block's last MFMA, B double buffered); loads of k-step t+3 into the stage that held t-1.
+  auto step = [&](auto p, int t) {
+    constexpr int P = decltype(p)::value;
+    const bf16x8(&fbc)[HNB] = (P & 1) ? fb1 : fb0;
+    bf16x8(&fbn)[HNB] = (P & 1) ? fb0 : fb1;
+    const u16* Sn = stg(IC<P + 1>{});
+    u16* Sd = stg(IC<P + 3>{});
+    asm volatile("" : "+v"(loff));
+    __builtin_amdgcn_s_waitcnt(kWaitNext);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < HMB * HNB; ++i) {
+      const int mb = i / HNB, nb = i % HNB;
+      acc[mb][nb] = mfma16(fa[mb], fbc[nb], acc[mb][nb]);
+      if (i < HNB) fbn[i] = fragB(Sn, i);
+      if (nb == HNB - 1) fa[mb] = fragA(Sn, mb);
+      if ((i & 7) == 0) dma(Sd, t + 3, i >> 3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+#pragma unroll
+  for (int j = 0; j < 4; ++j) dma(s0, 0, j);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) dma(s1, 1, j);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) dma(s2, 2, j);
+  __builtin_amdgcn_s_waitcnt(8 | (7 << 4));
+  __syncthreads();
+#pragma unroll
+  for (int mb = 0; mb < HMB; ++mb) fa[mb] = fragA(s0, mb);
+#pragma unroll
+  for (int nb = 0; nb < HNB; ++nb) fb0[nb] = fragB(s0, nb);
+  int t = 0;
+  for (; t + PNST <= nsteps; t += PNST) {
+    step(IC<0>{}, t);
+    step(IC<1>{}, t + 1);
+    step(IC<2>{}, t + 2);
+    step(IC<3>{}, t + 3);
+  }
+  if (t < nsteps) step(IC<0>{}, t);
+  if (t + 1 < nsteps) step(IC<1>{}, t + 1);
+  if (t + 2 < nsteps) step(IC<2>{}, t + 2);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  epi(acc, g, tm, tm * GBM + wm * GTM, tn * GBN + wn * GTN, lane, s0);
 }
 
 // ------------------------------------------------------------------ FP8 path
@@ -942,10 +1182,45 @@ hipError_t launch_linear(int dtype, const void* x, const void* w, void* y, int M
   return hipGetLastError();
 }
 
+size_t packed_rows_bytes(int64_t rows, int cols) {
+  return size_t((rows + PK_ROWS - 1) / PK_ROWS) * PK_ROWS * size_t(cols) * 2;
+}
+
+hipError_t launch_pack_rows(const void* x, int64_t rows, int cols, int64_t ldx, void* out,
+                            hipStream_t s) {
+  const int64_t tiles = (rows + PK_ROWS - 1) / PK_ROWS;
+  const int64_t n_chunks = tiles * PK_ROWS * (cols / PK_K) * 4;
+  if (n_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_rows_kernel, dim3(unsigned((n_chunks + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const u16*>(x), int(rows), cols, ldx, n_chunks,
+                     static_cast<u16*>(out));
+  return hipGetLastError();
+}
+
 hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
   if (a.N == 0) return hipSuccess;
   int n_vt;
-  if (a.dtype == CC_BF16) {
+  if (a.dtype == CC_BF16 && a.w_packed != nullptr) {
+    hipError_t err = launch_pack_rows(a.u, a.N, a.D, a.D, a.u_packed, s);
+    if (err != hipSuccess) return err;
+    GemmArgs g;
+    g.A2 = nullptr;
+    g.A = static_cast<const u16*>(a.w_packed);
+    g.B = static_cast<const u16*>(a.u_packed);
+    g.M = a.V;
+    g.N = a.N;
+    g.K = a.D;
+    g.lda = g.ldb = 0;   // unused: packed operands
+    g.tiles_n = (a.N + GBN - 1) / GBN;
+    n_vt = (a.V + GBM - 1) / GBM;
+    g.tiles_m = n_vt;
+    EpiLse16 e{a.partial};
+    hipLaunchKernelGGL(gemm_lmhead_packed<EpiLse16>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    hipLaunchKernelGGL(target_logit<u16>, dim3((a.N + 3) / 4), dim3(256), 0, s,
+                       static_cast<const u16*>(a.u), static_cast<const u16*>(a.w_lm), a.ids,
+                       a.target, a.N, a.D);
+  } else if (a.dtype == CC_BF16) {
     GemmArgs g;
     g.A2 = nullptr;
     g.A = static_cast<const u16*>(a.w_lm);

@@ -42,7 +42,7 @@ def _find(rows, pred):
 def main(fetch_dir: str, write_dir: str, out: str) -> None:
     f_rows = _per_dispatch(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
     w_rows = _per_dispatch(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
-    is_lm = lambda n: "gemm_tn_bf16" in n and "EpiLse" in n
+    is_lm = lambda n: "gemm_lmhead_packed" in n
     is_copy = lambda n: "copy" in n.lower() and "gemm" not in n and "compact" not in n
     # the copy is the last dispatch of the driver; take the largest copy-like dispatch
     f_copy = max(_find(f_rows, is_copy))
@@ -54,12 +54,14 @@ def main(fetch_dir: str, write_dir: str, out: str) -> None:
     with open(os.path.join(here, "csrc", "gemm.hip"), "rb") as fh:
         digest = hashlib.sha256(fh.read()).hexdigest()
     rec = {
-        "kernel": "gemm_tn_bf16<EpiLse> (LM head + fused log-sum-exp), C2 shapes",
+        "kernel": "gemm_lmhead_packed<EpiLse16> (LM head on packed operands + fused "
+                  "log-sum-exp), C2 shapes",
         "fetch_kib_raw": f_lm, "write_kib_raw": w_lm,
         "copy_fetch_kib_raw": f_copy, "copy_write_kib_raw": w_copy,
         "fetch_scale": kf, "write_scale": kw,
         "bytes_per_launch": (f_lm * kf + w_lm * kw) * 1024.0,
-        "algorithmic_bytes": "W_lm 128256x4096 bf16 (1.05 GB) + U 4096x4096 bf16 (33.6 MB) read, "
+        "algorithmic_bytes": "W_lm 128256x4096 bf16 (1.05 GB) + U 4096x4096 bf16 (33.6 MB) read "
+                             "(both packed), "
                              "partials 501x4096x8 B (16.4 MB) written",
         "gemm_source_sha256": digest,
     }

@@ -146,14 +146,18 @@ class Workload:
                                        seq_stride=L * hkv * cap * d, layer_stride=hkv * cap * d,
                                        head_stride=cap * d, tok_stride=d)
 
-    def inputs(self) -> cc.Inputs:
+    def inputs(self, w_lm_packed=None) -> cc.Inputs:
+        """cc_score inputs; w_lm_packed (cc_pack_lmhead of w_lm) for a packed problem."""
         if self.cfg.mode == "last_layer_h":
             return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=self.w_lm, layers=self.layers,
-                             final_norm=self.final_norm, h_last=self.h_last)
+                             final_norm=self.final_norm, h_last=self.h_last,
+                             w_lm_packed=w_lm_packed)
         if self.cfg.mode == "full":
             return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=self.w_lm, embed=self.embed,
-                             layers=self.layers, final_norm=self.final_norm)
-        return cc.inputs(q=self.q, kv=self.kv, token_ids=self.ids, w_o=self.w_o, w_lm=self.w_lm)
+                             layers=self.layers, final_norm=self.final_norm,
+                             w_lm_packed=w_lm_packed)
+        return cc.inputs(q=self.q, kv=self.kv, token_ids=self.ids, w_o=self.w_o, w_lm=self.w_lm,
+                         w_lm_packed=w_lm_packed)
 
     def keep_budget(self) -> list:
         return list(self.cfg.keep)

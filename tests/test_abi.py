@@ -183,3 +183,48 @@ def test_fused_and_fp8_entry_points_validate_on_the_host():
                                    dummy, big, None) == cc.CC_ERR_ARG    # no scale
     assert lib.cc_lmhead_score_fp8(ctypes.byref(p), dummy, dummy, dummy, dummy, dummy, None,
                                    dummy, 64, None) == cc.CC_ERR_WORKSPACE
+
+
+def test_packed_lmhead_entry_points_validate_on_the_host():
+    """The packed LM head's queries are host-only, and its entry points reject bad shapes,
+    dtypes, alignments, overlaps and missing packed weights before anything is enqueued."""
+    from paper_2607_27600_amd import cc
+    lib = cc._lib
+    n = ctypes.c_size_t(0)
+    dummy = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1002)
+    # packed size: rows rounded up to 256
+    assert lib.cc_pack_lmhead_bytes(300, 64, ctypes.byref(n)) == cc.CC_OK
+    assert n.value == 512 * 64 * 2
+    assert lib.cc_pack_lmhead_bytes(256, 96, ctypes.byref(n)) == cc.CC_OK and n.value == 256 * 96 * 2
+    assert lib.cc_pack_lmhead_bytes(0, 32, ctypes.byref(n)) == cc.CC_OK and n.value == 0
+    assert lib.cc_pack_lmhead_bytes(10, 48, ctypes.byref(n)) == cc.CC_ERR_ARG     # cols % 32
+    assert lib.cc_pack_lmhead_bytes(-1, 32, ctypes.byref(n)) == cc.CC_ERR_ARG
+    big = ctypes.c_size_t(1 << 30)
+    far = ctypes.c_void_p(0x10000000)
+    assert lib.cc_pack_lmhead(dummy, 10, 32, odd, big, None) == cc.CC_ERR_ARG     # alignment
+    assert lib.cc_pack_lmhead(None, 10, 32, far, big, None) == cc.CC_ERR_ARG
+    assert lib.cc_pack_lmhead(dummy, 10, 32, far, 1024, None) == cc.CC_ERR_WORKSPACE
+    assert lib.cc_pack_lmhead(dummy, 10, 32, ctypes.c_void_p(0x1100), big, None) == cc.CC_ERR_ARG  # overlap
+    assert lib.cc_pack_lmhead(None, 0, 32, None, 0, None) == cc.CC_OK
+    # problems: packed is bf16 only, a 0/1 flag, and adds the packed rows to the workspace
+    p, _k = _prob(lmhead_packed=1)
+    assert lib.cc_lmhead_workspace(ctypes.byref(p), ctypes.byref(n)) == cc.CC_OK
+    packed_ws = n.value
+    p0, _k0 = _prob()
+    assert lib.cc_lmhead_workspace(ctypes.byref(p0), ctypes.byref(n)) == cc.CC_OK
+    assert packed_ws - n.value >= 256 * 4096 * 2              # 250 rows -> one 256-row tile
+    pf, _kf = _prob(lmhead_packed=1, dtype=cc.CC_F32)
+    assert lib.cc_lmhead_workspace(ctypes.byref(pf), ctypes.byref(n)) == cc.CC_ERR_UNSUPPORTED
+    p2, _k2 = _prob(lmhead_packed=2)
+    assert lib.cc_score_workspace(ctypes.byref(p2), ctypes.byref(n)) == cc.CC_ERR_ARG
+    # the packed sub-step needs a packed problem and weight; the row-major one refuses it
+    ws = ctypes.c_void_p(0x100000)
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p0), dummy, dummy, dummy, dummy, dummy, None,
+                                      ws, big, None) == cc.CC_ERR_ARG
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, dummy, None, dummy, dummy, None,
+                                      ws, big, None) == cc.CC_ERR_ARG
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, dummy, odd, dummy, dummy, None,
+                                      ws, big, None) == cc.CC_ERR_ARG
+    assert lib.cc_lmhead_score(ctypes.byref(p), dummy, dummy, dummy, dummy, None, ws, big,
+                               None) == cc.CC_ERR_ARG
