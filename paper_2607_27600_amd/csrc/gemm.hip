@@ -265,19 +265,33 @@ struct EpiSwiglu {
   }
 };
 
-// Workgroup -> output tile: groups of GROUP_M tile rows, walked with the row index
-// fastest, so the workgroups in flight on the chip cover a few rows of tiles (sharing the
-// A tiles) times many columns (sharing each B tile) and find most k-slices in L2.
-// (Partitioning the order by XCD measured no better.)
+// Workgroup -> output tile.  The tile grid is cut into supertiles of ST_M x ST_N tiles (rows
+// of supertiles first, each row walked left to right), and inside a supertile the workgroups
+// walk groups of GROUP_M tile rows with the row index fastest.  Workgroups are dealt to the
+// eight XCDs round robin, so each XCD's resident workgroups cover GROUP_M rows x 8 columns
+// of tiles (few distinct k-slices per k-step in its L2), and the whole chip works inside one
+// supertile at a time, whose operand rows (32 + 16 tiles of 256 rows) stay in the Infinity
+// Cache while the supertile row is swept: the wide operand is then re-read once per
+// supertile row instead of once per GROUP_M tile rows.  A grid of at most 16 tile columns is
+// the plain GROUP_M walk.  (Partitioning the order by XCD explicitly measured no better.)
 constexpr int GROUP_M = 4;
+constexpr int ST_M = 32, ST_N = 16;
 
 __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int group = bid / (GROUP_M * tiles_n);
+  const int sr = bid / (ST_M * tiles_n);
+  const int rem = bid - sr * (ST_M * tiles_n);
+  const int m0 = sr * ST_M;
+  const int sm = min(ST_M, tiles_m - m0);        // tile rows in this supertile row
+  const int sc = rem / (sm * ST_N);
+  const int rem2 = rem - sc * (sm * ST_N);
+  const int n0 = sc * ST_N;
+  const int sn = min(ST_N, tiles_n - n0);        // tile columns in this supertile
+  const int group = rem2 / (GROUP_M * sn);
   const int first = group * GROUP_M;
-  const int gsize = min(GROUP_M, tiles_m - first);
-  const int within = bid - group * GROUP_M * tiles_n;
-  tm = first + within % gsize;
-  tn = within / gsize;
+  const int gsize = min(GROUP_M, sm - first);
+  const int within = rem2 - group * (GROUP_M * sn);
+  tm = m0 + first + within % gsize;
+  tn = n0 + within / gsize;
 }
 
 // Scheduling hints: interleave MFMAs with LDS reads / writes / global loads so the matrix
