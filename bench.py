@@ -246,6 +246,7 @@ def bench_loop(args, dev) -> dict:
     appends are copies of the stream's next entries."""
     import numpy as np
     import torch
+    from paper_2607_27600_amd import cc
     from paper_2607_27600_amd.refresh import Model, RefreshLoop, run_stream
     from synth import gen
     L, hq, hkv, d, D, F, V = 28, 28, 4, 128, 3584, 18944, 152064
@@ -258,6 +259,7 @@ def bench_loop(args, dev) -> dict:
                  w_gate=wt(3, (F, D)), w_up=wt(4, (F, D)), w_down=wt(5, (D, F)))
     m = Model(mode="last_layer_h", n_layers=L, n_heads_q=hq, n_heads_kv=hkv, head_dim=d,
               hidden=D, vocab=V, w_lm=wt(6, (V, D)), layer=layer, final_norm=ones, ffn=F)
+    m.w_lm_packed = cc.cc_pack_lmhead(m.w_lm)      # packed once per model
     S_k = up(gen.normal_bf16(0, 20010, (L, hkv, T_total, d)))
     S_v = up(gen.normal_bf16(0, 20011, (L, hkv, T_total, d)))
     S_h = up(gen.normal_bf16(0, 20012, (T_total, D)))
@@ -299,7 +301,8 @@ def bench_loop(args, dev) -> dict:
         "n_gpus": 1, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "LOOP: Qwen2.5-7B shapes, exact fast variant, J=512, h=256, "
                                "4096-token prompt + 1024 decoded tokens",
-                   "J": J, "h": h, "cache_layers": L, "prompt": T_prompt, "total": T_total},
+                   "J": J, "h": h, "cache_layers": L, "prompt": T_prompt, "total": T_total,
+                   "lmhead": "packed"},
         "refreshes": len(ref_ms), "refresh_ms_min": float(np.min(ref_ms)),
         "refresh_ms_median": float(np.median(ref_ms)),
         "stream_wall_s": wall, "amortised_refresh_us_per_token": float(np.sum(ref_ms)) * 1e3 / T_total,

@@ -41,6 +41,7 @@ class Model:
     ffn: int = 0
     rope_theta: float = 5e5
     rms_eps: float = 1e-5
+    w_lm_packed: Optional[torch.Tensor] = None  # cc_pack_lmhead(w_lm): the packed LM head
 
     @property
     def row_width(self) -> int:
@@ -94,15 +95,17 @@ class RefreshLoop:
         return cc.problem(dtype="bf16", cu_seqlens=[0, self.n], n_heads_q=m.n_heads_q,
                           n_heads_kv=m.n_heads_kv, head_dim=m.head_dim, hidden=m.hidden,
                           vocab=m.vocab, device=self.device, mode=m.mode, ffn=m.ffn,
-                          rope_theta=m.rope_theta, rms_eps=m.rms_eps)
+                          rope_theta=m.rope_theta, rms_eps=m.rms_eps,
+                          lmhead_packed=m.w_lm_packed is not None)
 
     def inputs(self) -> cc.Inputs:
         m, n = self.m, self.n
         if m.mode in ("last_layer", "last_layer_fused"):
             return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=m.w_lm, w_o=m.w_o,
-                             q=self.rows[:n])
+                             q=self.rows[:n], w_lm_packed=m.w_lm_packed)
         return cc.inputs(kv=self.kv, token_ids=self.ids, w_lm=m.w_lm, layers=[m.layer],
-                         final_norm=m.final_norm, h_last=self.rows[:n], pos_ids=self.pos)
+                         final_norm=m.final_norm, h_last=self.rows[:n], pos_ids=self.pos,
+                         w_lm_packed=m.w_lm_packed)
 
     def scores(self) -> torch.Tensor:
         """Counter-causal surprise of every cached entry (the last one is +inf)."""

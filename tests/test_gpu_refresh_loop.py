@@ -29,7 +29,7 @@ def _stream(T, width, seed=3):
                 ids=r.integers(0, V, T).astype(np.int32))
 
 
-def _model(mode):
+def _model(mode, packed=False):
     from paper_2607_27600_amd.refresh import Model
     w = lambda tid, shape: gen.normal_bf16(7, tid, shape, 0.05)
     host = dict(w_lm=w(1, (V, D)), w_o=w(2, (D, HQ * D_HEAD)),
@@ -46,6 +46,9 @@ def _model(mode):
               vocab=V, w_lm=w_lm, w_o=dev(host["w_o"]),
               layer={k: dev(v) for k, v in host["layer"].items()},
               final_norm=dev(host["final_norm"]), ffn=F, rope_theta=THETA, rms_eps=EPS)
+    if packed:
+        from paper_2607_27600_amd import cc
+        m.w_lm_packed = cc.cc_pack_lmhead(w_lm)
     return m, host
 
 
@@ -65,13 +68,17 @@ def _state(loop):
                 ids=loop.ids.cpu().numpy().copy(), pos=loop.pos.cpu().numpy().copy())
 
 
-@pytest.mark.parametrize("mode,chunked", [("last_layer_h", True), ("last_layer", True),
-                                          ("last_layer_h", False), ("last_layer_fused", True)])
-def test_refresh_loop(mode, chunked):
+@pytest.mark.parametrize("mode,chunked,packed", [("last_layer_h", True, False),
+                                                 ("last_layer", True, False),
+                                                 ("last_layer_h", False, False),
+                                                 ("last_layer_fused", True, False),
+                                                 ("last_layer_h", True, True),
+                                                 ("last_layer_fused", True, True)])
+def test_refresh_loop(mode, chunked, packed):
     from paper_2607_27600_amd.refresh import RefreshLoop, run_stream
-    print(f"[refresh loop] mode={mode} chunked={chunked}", flush=True)
+    print(f"[refresh loop] mode={mode} chunked={chunked} packed={packed}", flush=True)
     J, h, T_prompt, T_total = 40, 16, 100, 170
-    m, host = _model(mode)
+    m, host = _model(mode, packed)
     cap = None if chunked else T_total
     loop = RefreshLoop(m, J, h, capacity=cap)
     S = _stream(T_total, m.row_width)
