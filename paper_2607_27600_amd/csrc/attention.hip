@@ -383,17 +383,33 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (valid) {
-    u16* op = a.o + (int64_t(seq0 + pos) * a.hq + hq) * HD + hi * 4;
+  // The output goes out through LDS as whole rows.  The K buffers are free here (the last
+  // step waited for every load and ended with a barrier); each wave stages its 32 rows x 128
+  // dims (8 KB, 16-byte chunk c of row r at chunk c ^ (r & 15), so both the 8-byte writes of
+  // the lane halves and the 16-byte row reads hit every bank once), then writes 16 bytes per
+  // lane along the rows.  The g rows of one position are adjacent in o (head-major), so a
+  // wave instruction stores 1 KB of whole rows instead of 64 scattered 8-byte pieces.  LDS
+  // operations of one wave complete in order, so the wave needs no barrier of its own.
+  char* stg = reinterpret_cast<char*>(wave < 2 ? kl0 : kl1) + (wave & 1) * (ROWS_W * HD * 2);
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+  for (int db = 0; db < 4; ++db)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        bf16x4 o;
+    for (int jj = 0; jj < 4; ++jj) {
+      bf16x4 o;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (__bf16)(acc[db][jj * 4 + e] * inv);
-        *reinterpret_cast<bf16x4*>(op + db * 32 + jj * 8) = o;
-      }
+      for (int e = 0; e < 4; ++e) o[e] = (__bf16)(acc[db][jj * 4 + e] * inv);
+      const int c = db * 4 + jj;
+      *reinterpret_cast<bf16x4*>(stg + col * (HD * 2) + ((c ^ (col & 15)) * 16) + hi * 8) = o;
+    }
+#pragma unroll
+  for (int i = 0; i < ROWS_W / 4; ++i) {
+    const int r = 4 * i + (lane >> 4), c = lane & 15;
+    const uint4 v = *reinterpret_cast<const uint4*>(stg + r * (HD * 2) + ((c ^ (r & 15)) * 16));
+    const int orow = rb * ROWS + wave * ROWS_W + r;
+    if (orow < nrows) {
+      const int opos = orow / g, ohq = kvh * g + orow % g;
+      *reinterpret_cast<uint4*>(a.o + (int64_t(seq0 + opos) * a.hq + ohq) * HD + c * 8) = v;
+    }
   }
 }
 
