@@ -263,7 +263,7 @@ cc_status cc_pack_lmhead_bytes(int64_t rows, int32_t cols, size_t* bytes);
 /* Packs a bf16 matrix x [rows][cols] (row stride cols; cols a positive multiple of 32;
  * x 16-byte aligned) into the layout the packed LM head stages: for each 256-row tile
  * and 32-column step, one 16 KB block in which row r (64 bytes at 64r) holds its
- * 16-byte chunk c (columns 8c .. 8c+7 of the step) at chunk position c ^ ((r >> 2) & 3);
+ * 16-byte chunk c (columns 8c .. 8c+7 of the step) at chunk position c ^ ((r >> 1) & 3);
  * rows past `rows` are zero.  A bit copy that changes the layout only: the weight
  * preparation for lmhead_packed = 1, made once per model (the LM-head input rows are
  * packed inside each call).  out: device, cc_pack_lmhead_bytes bytes, 16-byte aligned,

@@ -4,6 +4,11 @@
     rocprofv3 --pmc WRITE_SIZE -d <dir_write> -o run --output-format csv -- python bench.py --pmc-driver
     python -m paper_2607_27600_amd.pmc_summary <dir_fetch> <dir_write> profiles/lmhead_c2_traffic.json
 
+A third mode tabulates matrix-core utilisation per kernel from one run with the SQ/GRBM
+counters named in util():
+
+    python -m paper_2607_27600_amd.pmc_summary util <dir>
+
 FETCH_SIZE / WRITE_SIZE are in KiB per dispatch.  The driver also copies 1 GiB device to
 device; each counter is scaled by (1 GiB / what it reads for that copy), so the figures are
 calibrated against a transfer of known size.  The record carries the sha256 of gemm.hip;
@@ -70,5 +75,44 @@ def main(fetch_dir: str, write_dir: str, out: str) -> None:
     print(json.dumps(rec, indent=1))
 
 
+def _all_counters(path: str) -> list:
+    """Per dispatch: (id, kernel name, {counter: value summed over instances})."""
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            k = int(r["Dispatch_Id"])
+            name, vals = out.setdefault(k, (r["Kernel_Name"], {}))
+            vals[r["Counter_Name"]] = vals.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [(k, *out[k]) for k in sorted(out)]
+
+
+def util(run_dir: str, n_xcc: int = 8, n_simd: int = 1024, n_cu: int = 256) -> None:
+    """Matrix-core utilisation per kernel from a run with SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 and GRBM_GUI_ACTIVE.
+
+    GRBM_GUI_ACTIVE sums the eight XCDs' own clocks, so the kernel's cycle count is the sum
+    over n_xcc; SQ_VALU_MFMA_BUSY_CYCLES sums busy cycles over every SIMD; each MOPS unit is
+    512 FLOP.  Utilisation = busy / (cycles x SIMDs).  SQ_LDS_BANK_CONFLICT counts cycles in
+    which a CU's LDS stalls on bank conflicts, reported per CU-cycle as rocprof's own
+    LDSBankConflict metric does.
+    """
+    rows = _all_counters(os.path.join(run_dir, "run_counter_collection.csv"))
+    print("| dispatch | kernel | cycles | MFMA FLOP | MFMA busy | VALU active / wave-cycle | LDS bank-conflict stall / CU-cycle |")
+    print("|---|---|---|---|---|---|---|")
+    for k, name, c in rows:
+        busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        if busy == 0.0:
+            continue
+        cyc = c["GRBM_GUI_ACTIVE"] / n_xcc
+        short = name.replace("cc::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        valu = c.get("SQ_ACTIVE_INST_VALU", 0.0) / max(c.get("SQ_WAVE_CYCLES", 1.0), 1.0)
+        lds = c.get("SQ_LDS_BANK_CONFLICT", 0.0) / (cyc * n_cu)
+        print(f"| {k} | `{short}` | {cyc:.4g} | {c.get('SQ_INSTS_VALU_MFMA_MOPS_BF16', 0.0) * 512:.4g} "
+              f"| {100 * busy / (cyc * n_simd):.1f}% | {valu:.2f} | {100 * lds:.1f}% |")
+
+
 if __name__ == "__main__":
-    main(*sys.argv[1:4])
+    if sys.argv[1] == "util":
+        util(sys.argv[2])
+    else:
+        main(*sys.argv[1:4])

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 def _packed_reference(x: np.ndarray) -> np.ndarray:
     """uint16 [R][K] -> the packed layout as uint16, from its definition: per 256-row tile
     t and 32-column step s a block of 256 rows x 32; row r holds its 8-element chunk c at
-    chunk position c ^ ((r >> 2) & 3); rows past R are zero."""
+    chunk position c ^ ((r >> 1) & 3); rows past R are zero."""
     R, K = x.shape
     T, S = (R + 255) // 256, K // 32
     xp = np.zeros((T * 256, K), dtype=np.uint16)
@@ -30,7 +30,7 @@ def _packed_reference(x: np.ndarray) -> np.ndarray:
     out = np.zeros((T, S, 256, 4, 8), dtype=np.uint16)
     for r in range(256):
         for c in range(4):
-            out[:, :, r, c ^ ((r >> 2) & 3), :] = blocks[:, r, :, c, :]
+            out[:, :, r, c ^ ((r >> 1) & 3), :] = blocks[:, r, :, c, :]
     return out.reshape(-1)
 
 
