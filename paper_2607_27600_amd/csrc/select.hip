@@ -130,28 +130,47 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------ register path
-// Segments of up to RMAX scores: the workgroup reads its segment once, coalesced, into
-// registers (score j*RNT + t in slot j of thread t) and never touches it again.  The
-// radix passes run on rel = key - kmin (kmin, kmax: the segment's extreme keys) over the
-// B = bit length of kmax - kmin bits, so the first digit spreads over the scores' actual
-// range instead of the few sign and exponent patterns they share.  Histograms are private
-// to each wave (fewer colliding LDS atomics) and double buffered (the next pass's buffer
-// is cleared while this one is reduced).  The emission ranks ties and kept entries in
-// index order from per-(wave, slot) ballot counts, scanned once per kind.
+// Segments of up to RMAX scores: the workgroup reads its segment once into registers and
+// never touches it again.  The segment is cut into 8 chunks of 4096 scores; thread t of
+// 1024 holds scores 4t .. 4t+3 of every chunk (one 16-byte load per chunk, 1 KB per wave
+// instruction), so index order is (chunk, thread, slot).
+//  - Extremes: kmin over the segment, kmaxf over its keys other than +inf, and the number
+//    of +inf keys.  When the +inf keys fill the budget they hold the threshold.  Otherwise
+//    the radix digits run on rel = key - kmin over the B = bit length of kmaxf - kmin
+//    bits, so the first digit spreads over the finite scores' actual range (the +inf of a
+//    sequence's last entry would otherwise squeeze them all into one bucket).
+//  - One 8-bit pass over every key (per-wave LDS histograms).  When the bucket that holds
+//    the threshold has at most CMAX keys, their low bits are copied to LDS and one wave
+//    finishes the lower digits on that list, with no further block-wide barriers;
+//    otherwise further block-wide passes run over the registers.
+//  - Emission: a thread's flagged keys per chunk are counted, and one batched scan over
+//    the workgroup (8 chunk counts per thread, two per word) gives every flagged key its
+//    rank in index order: first for the ties (when not all of them are kept), then for
+//    the kept keys, which are written at their ranks.
 constexpr int RNT = 1024;
 constexpr int RWAVES = RNT / 64;
-constexpr int RPT = 32;
+constexpr int RCW = 4;                 // scores per thread per chunk
+constexpr int RCH = 8;                 // chunks
+constexpr int RCHUNK = RNT * RCW;      // scores per chunk
+constexpr int RPT = RCH * RCW;         // scores per thread
 constexpr int RMAX = RNT * RPT;
+constexpr int CMAX = 4096;
+constexpr uint32_t KINF = 0xff800000u;   // order_key(+inf): the largest key
 
-// Exclusive scan, in place, of tab[w][j] in (slot j, wave w) order; run by wave 0.
-__device__ __forceinline__ void scan_slots(uint32_t (*tab)[RPT], int lane) {
-  // lane l takes slots j = l/2 (waves 8*(l&1) .. +7): consecutive lanes follow the order
-  const int j = lane >> 1, w0 = (lane & 1) * 8;
-  uint32_t v[8], sum = 0u;
+struct Pick {
+  uint32_t digit, rem, cnt;
+};
+
+// Run by one whole wave: in a 256-bin histogram searched from the highest digit down, the
+// bin holding the rem-th largest counted key (1 <= rem <= total), the rank left inside it
+// and its count; every lane receives the result.
+__device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int lane) {
+  // lane l owns digits 255-4l .. 252-4l (descending)
+  uint32_t c[4], sum = 0u;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    v[i] = tab[w0 + i][j];
-    sum += v[i];
+  for (int q = 0; q < 4; ++q) {
+    c[q] = h[255 - 4 * lane - q];
+    sum += c[q];
   }
   uint32_t incl = sum;
 #pragma unroll
@@ -159,22 +178,78 @@ __device__ __forceinline__ void scan_slots(uint32_t (*tab)[RPT], int lane) {
     const uint32_t t = __shfl_up(incl, off);
     if (lane >= off) incl += t;
   }
-  uint32_t run = incl - sum;
+  const uint32_t excl = incl - sum;
+  const bool mine = excl < rem && incl >= rem;
+  uint32_t digit = 0u, r = 0u, cn = 0u, acc = excl;
+  bool done = false;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    tab[w0 + i][j] = run;
-    run += v[i];
+  for (int q = 0; q < 4; ++q) {
+    if (mine && !done && acc + c[q] >= rem) {
+      digit = uint32_t(255 - 4 * lane - q);
+      r = rem - acc;
+      cn = c[q];
+      done = true;
+    }
+    acc += c[q];
+  }
+  const uint64_t bal = __ballot(mine);
+  const int src = bal ? __builtin_ctzll(bal) : 0;
+  return {uint32_t(__shfl(int(digit), src)), uint32_t(__shfl(int(r), src)),
+          uint32_t(__shfl(int(cn), src))};
+}
+
+// Ranks in index order of the keys flagged in m (bit 4c + i: slot i of chunk c): base[c]
+// = flagged keys before this thread's part of chunk c.  wtot: [RWAVES][RCH / 2] words of
+// LDS owned by this call.  Contains one barrier.
+__device__ __forceinline__ void chunk_offsets(uint64_t m, uint32_t (&base)[RCH],
+                                              uint32_t (*wtot)[RCH / 2], int lane, int wave) {
+  uint32_t own[RCH / 2], inc[RCH / 2];
+#pragma unroll
+  for (int q = 0; q < RCH / 2; ++q) {
+    own[q] = uint32_t(__popcll((m >> (8 * q)) & 0xfull)) |
+             (uint32_t(__popcll((m >> (8 * q + 4)) & 0xfull)) << 16);
+    inc[q] = own[q];
+  }
+  // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1)
+#pragma unroll
+    for (int q = 0; q < RCH / 2; ++q) {
+      const uint32_t t = uint32_t(__shfl_up(int(inc[q]), off));
+      if (lane >= off) inc[q] += t;
+    }
+  if (lane == 63)
+#pragma unroll
+    for (int q = 0; q < RCH / 2; ++q) wtot[wave][q] = inc[q];
+  __syncthreads();
+  uint32_t run = 0u;
+#pragma unroll
+  for (int q = 0; q < RCH / 2; ++q) {
+    uint32_t all = 0u, before = 0u;
+#pragma unroll
+    for (int w = 0; w < RWAVES; ++w) {
+      const uint32_t t = wtot[w][q];
+      all += t;
+      before += w < wave ? t : 0u;
+    }
+    const uint32_t mine = before + inc[q] - own[q];
+    base[2 * q] = run + (mine & 0xffffu);
+    run += all & 0xffffu;
+    base[2 * q + 1] = run + (mine >> 16);
+    run += all >> 16;
   }
 }
 
-__global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restrict__ scores,
+__global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restrict__ scores,
                                                            const SelSeg* __restrict__ segs,
                                                            int32_t* __restrict__ keep) {
   __shared__ uint32_t hist[2][RWAVES][256];
   __shared__ uint32_t tot[256];
-  __shared__ __attribute__((aligned(16))) uint32_t tab[RWAVES][RPT];
-  __shared__ uint32_t red[2][RWAVES];
-  __shared__ uint32_t sh_digit, sh_rem, sh_cnt;
+  __shared__ uint32_t cand[CMAX];
+  __shared__ uint32_t whist[256];
+  __shared__ uint32_t red[3][RWAVES];
+  __shared__ uint32_t wtot[2][RWAVES][RCH / 2];
+  __shared__ uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
   const SelSeg sg = segs[blockIdx.x];
   const int n = sg.len, k = sg.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -184,169 +259,241 @@ __global__ __launch_bounds__(RNT, 2) void select_keep_regs(const float* __restri
     for (int i = tid; i < n; i += RNT) out[i] = i;
     return;
   }
-  // one coalesced read (indices past the end re-read the last score; they never count)
-  const float* s = scores + sg.start;
+  // key[4c + i] = score c * RCHUNK + 4 * tid + i, read from a uniform base plus a 32-bit
+  // byte offset.  With a 16-byte aligned start and a length divisible by four, one 16-byte
+  // load per chunk (chunks past the end re-read the last four scores); otherwise four
+  // loads per chunk (indices past the end re-read the last score).  Keys past the end are
+  // marked padding below.
+  const char* sb = reinterpret_cast<const char*>(scores + sg.start);
   uint32_t key[RPT];
+  int t4 = 4 * tid;
+  if ((reinterpret_cast<uintptr_t>(sb) & 15u) == 0u && (n & 3) == 0) {
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) key[j] = __float_as_uint(s[min(j * RNT + tid, n - 1)]);
+    for (int c = 0; c < RCH; ++c) {
+      const uint32_t off = uint32_t(min(c * RCHUNK + t4, n - 4)) * 4u;
+      const uint4 v = *reinterpret_cast<const uint4*>(sb + off);
+      key[4 * c] = v.x;
+      key[4 * c + 1] = v.y;
+      key[4 * c + 2] = v.z;
+      key[4 * c + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const uint32_t off = uint32_t(min((j >> 2) * RCHUNK + t4 + (j & 3), n - 1)) * 4u;
+      key[j] = *reinterpret_cast<const uint32_t*>(sb + off);
+    }
+  }
 #pragma unroll
   for (int j = 0; j < RPT; ++j) key[j] = order_key(__uint_as_float(key[j]));
-  const int nvalid = min(RPT, max(0, (n - tid + RNT - 1) / RNT));   // slots j < nvalid hold scores
-  auto valid = [&](int j) { return j < nvalid; };
-
-  // extreme keys of the segment; the first histogram buffer is cleared meanwhile
-  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  // Index arithmetic restarts from an opaque copy of 4*tid here and before the stores, so
+  // the compiler recomputes it instead of keeping 64 indices (and their compare masks)
+  // live across the kernel.  vbits: bit j set when key j lies inside the segment.
+  asm volatile("" : "+v"(t4));
+  uint64_t vbits = 0u;
 #pragma unroll
-  for (int j = 0; j < RPT; ++j)
-    if (valid(j)) {
-      kmin = min(kmin, key[j]);
-      kmax = max(kmax, key[j]);
-    }
+  for (int c = 0; c < RCH; ++c) {
+    // slots i < n - (c * RCHUNK + 4 tid) of chunk c hold scores
+    const int nv = min(max(n - c * RCHUNK - t4, 0), RCW);
+    vbits |= uint64_t((1u << nv) - 1u) << (RCW * c);
+  }
+  auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
+
+  // extremes of the segment and its number of +inf keys; the first histogram buffer is
+  // cleared meanwhile
+  uint32_t kmin = 0xffffffffu, kmaxf = 0u, ninf = 0u;
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const bool v = valid(j), inf = key[j] == KINF;
+    kmin = v ? min(kmin, key[j]) : kmin;
+    kmaxf = v && !inf ? max(kmaxf, key[j]) : kmaxf;
+    ninf += uint32_t(v && inf);
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
-    kmin = min(kmin, uint32_t(__shfl_xor(kmin, off)));
-    kmax = max(kmax, uint32_t(__shfl_xor(kmax, off)));
+    kmin = min(kmin, uint32_t(__shfl_xor(int(kmin), off)));
+    kmaxf = max(kmaxf, uint32_t(__shfl_xor(int(kmaxf), off)));
+    ninf += uint32_t(__shfl_xor(int(ninf), off));
   }
   if (lane == 0) {
     red[0][wave] = kmin;
-    red[1][wave] = kmax;
+    red[1][wave] = kmaxf;
+    red[2][wave] = ninf;
   }
   for (int i = tid; i < RWAVES * 256; i += RNT) (&hist[0][0][0])[i] = 0u;
+  if (tid == 0) sh_ncand = 0u;
   __syncthreads();
   kmin = red[0][0];
-  kmax = red[1][0];
+  kmaxf = red[1][0];
+  ninf = red[2][0];
 #pragma unroll
   for (int w = 1; w < RWAVES; ++w) {
     kmin = min(kmin, red[0][w]);
-    kmax = max(kmax, red[1][w]);
+    kmaxf = max(kmaxf, red[1][w]);
+    ninf += red[2][w];
   }
-  const uint32_t range = kmax - kmin;
-  const int B = range ? 32 - __clz(range) : 0;
-  // Slots at or past jmax hold no score for any thread and are skipped (a uniform test).
-  // The padding of the last, partial slot becomes copies of the smallest key: it is last
-  // in index order, and since k < n the kept ties (lowest index first) never reach it, so
-  // it changes no selection.
-  const int jmax = (n + RNT - 1) / RNT;
+  // From here on the registers hold rel = key - kmin: the order is unchanged and +inf
+  // keys are the ones equal to rinf.  Padding (indices past the end) becomes rel 0, the
+  // smallest key: it is last in index order, and since k < n the kept ties (lowest index
+  // first) never reach it, so it changes no selection; counts below may include it.
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? key[j] : kmin;
+  for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? key[j] - kmin : 0u;
+  const uint32_t rinf = KINF - kmin;
 
-  // radix passes, 8 bits at a time from bit B down; `prefix` holds rel >> hi
-  uint32_t prefix = 0u, rem = uint32_t(k);
-  int buf = 0;
-  for (int hi = B; hi > 0; buf ^= 1) {
-    const int lo = hi > 8 ? hi - 8 : 0;
-    const uint32_t dmask = (1u << (hi - lo)) - 1u;
-    uint32_t(*h)[256] = hist[buf];
+  // T: the k-th largest rel; keep `rem` of the keys equal to T, of which there are `cnt`
+  // (a count that may include padding)
+  uint32_t T, rem, cnt;
+  if (ninf >= uint32_t(k)) {
+    T = rinf;
+    rem = uint32_t(k);
+    cnt = ninf;
+  } else {
+    // at least one key is below +inf, so kmin <= kmaxf
+    rem = uint32_t(k) - ninf;
+    const uint32_t range = kmaxf - kmin;
+    const int B = range ? 32 - __clz(range) : 0;
+    uint32_t prefix = 0u;   // rel >> hi of the keys still in the running
+    if (B == 0) {
+      cnt = uint32_t(n) - ninf;   // every key below +inf equals kmin
+    } else {
+      int hi = B, buf = 0;
+      bool first = true;
+      while (hi > 0) {
+        const int lo = hi > 8 ? hi - 8 : 0;
+        const uint32_t dmask = (1u << (hi - lo)) - 1u;
+        uint32_t(*h)[256] = hist[buf];
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const uint32_t rel = key[j] - kmin;
-      const uint32_t top = hi >= 32 ? 0u : rel >> hi;
-      if (j < jmax && top == prefix) atomicAdd(&h[wave][(rel >> lo) & dmask], 1u);
-    }
-    __syncthreads();
-    if (tid < 256) {
-      uint32_t t = 0u;
-#pragma unroll
-      for (int w = 0; w < RWAVES; ++w) t += h[w][tid];
-      tot[tid] = t;
-    }
-    for (int i = tid; i < RWAVES * 256; i += RNT) (&hist[buf ^ 1][0][0])[i] = 0u;
-    __syncthreads();
-    if (tid < 64) {
-      // lane l owns digits 255-4l .. 252-4l (descending); find the bucket holding the
-      // rem-th largest candidate
-      uint32_t c[4], sum = 0u;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        c[q] = tot[255 - 4 * lane - q];
-        sum += c[q];
-      }
-      uint32_t incl = sum;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t t = __shfl_up(incl, off);
-        if (lane >= off) incl += t;
-      }
-      const uint32_t excl = incl - sum;
-      if (excl < rem && incl >= rem) {
-        uint32_t acc = excl;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (acc + c[q] >= rem) {
-            sh_digit = uint32_t(255 - 4 * lane - q);
-            sh_rem = rem - acc;
-            sh_cnt = c[q];
-            break;
-          }
-          acc += c[q];
+        for (int j = 0; j < RPT; ++j) {
+          const uint32_t rel = key[j];
+          const uint32_t top = hi >= 32 ? 0u : rel >> hi;
+          if (rel != rinf && top == prefix) atomicAdd(&h[wave][(rel >> lo) & dmask], 1u);
+          __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 64 live masks
         }
+        __syncthreads();
+        if (tid < 256) {
+          uint32_t t = 0u;
+#pragma unroll
+          for (int w = 0; w < RWAVES; ++w) t += h[w][tid];
+          tot[tid] = t;
+        }
+        for (int i = tid; i < RWAVES * 256; i += RNT) (&hist[buf ^ 1][0][0])[i] = 0u;
+        __syncthreads();
+        if (wave == 0) {
+          const Pick p = pick_bucket(tot, rem, lane);
+          if (lane == 0) {
+            sh_digit = p.digit;
+            sh_rem = p.rem;
+            sh_cnt = p.cnt;
+          }
+        }
+        __syncthreads();
+        prefix = (prefix << (hi - lo)) | sh_digit;
+        rem = sh_rem;
+        cnt = sh_cnt;
+        hi = lo;
+        buf ^= 1;
+        if (first && hi > 0 && cnt <= uint32_t(CMAX)) {
+          // The `cnt` keys of the chosen bucket (rel >> hi == prefix) go to LDS as their
+          // low hi bits, each thread's after those of the lanes before it.
+          const int L = hi;
+          const uint32_t lmask = (1u << L) - 1u;
+          uint32_t mine = 0u;
+#pragma unroll
+          for (int j = 0; j < RPT; ++j) mine += uint32_t(key[j] != rinf && (key[j] >> L) == prefix);
+          uint32_t incl = mine;
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t t = uint32_t(__shfl_up(int(incl), off));
+            if (lane >= off) incl += t;
+          }
+          uint32_t base = 0u;
+          if (lane == 63) base = atomicAdd(&sh_ncand, incl);
+          uint32_t pos = uint32_t(__shfl(int(base), 63)) + incl - mine;
+#pragma unroll
+          for (int j = 0; j < RPT; ++j) {
+            const uint32_t rel = key[j];
+            if (rel != rinf && (rel >> L) == prefix) {
+              if (pos < uint32_t(CMAX)) cand[pos] = rel & lmask;
+              ++pos;
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          __syncthreads();
+          if (wave == 0) {
+            // radix passes of 8 bits over the list, by this wave alone: its LDS operations
+            // execute in program order, so the clears, the atomics and the reads of whist
+            // need no barrier (the waits and fences keep the compiler from moving them)
+            const int nc = int(min(cnt, uint32_t(CMAX)));
+            uint32_t p2 = 0u, r2 = rem, c2 = cnt;
+            int h2 = L;
+            while (h2 > 0) {
+              const int l2 = h2 > 8 ? h2 - 8 : 0;
+              const uint32_t m2 = (1u << (h2 - l2)) - 1u;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) whist[4 * lane + q] = 0u;
+              asm volatile("" ::: "memory");
+              for (int i = lane; i < nc; i += 64) {
+                const uint32_t v = cand[i];
+                if ((v >> h2) == p2) atomicAdd(&whist[(v >> l2) & m2], 1u);
+              }
+              __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+              asm volatile("" ::: "memory");
+              const Pick pk = pick_bucket(whist, r2, lane);
+              __builtin_amdgcn_s_waitcnt(0xc07f);
+              asm volatile("" ::: "memory");
+              p2 = (p2 << (h2 - l2)) | pk.digit;
+              r2 = pk.rem;
+              c2 = pk.cnt;
+              h2 = l2;
+            }
+            if (lane == 0) {
+              sh_digit = p2;
+              sh_rem = r2;
+              sh_cnt = c2;
+            }
+          }
+          __syncthreads();
+          prefix = (prefix << L) | sh_digit;
+          rem = sh_rem;
+          cnt = sh_cnt;
+          hi = 0;
+        }
+        first = false;
       }
     }
-    __syncthreads();
-    prefix = (prefix << (hi - lo)) | sh_digit;
-    rem = sh_rem;
-    hi = lo;
+    T = prefix;
   }
-  const uint32_t T = kmin + prefix;   // the k-th largest key; keep `rem` of the keys equal to T
-  // keys equal to T: the last pass's bucket (all keys when the range is 0).  The count may
-  // include padding copies of kmin, so equality with rem proves every tie is kept.
-  const bool all_ties = B > 0 && sh_cnt == rem;
+  // every tie is kept when their count equals the number still to keep (a count that
+  // includes padding cannot: real ties alone already reach rem)
+  const bool all_ties = cnt == rem;
 
-  // ranks in index order: element (j, t) comes after every element of slots < j and after
-  // (j, t') for t' < t.  A wave's count per slot is a ballot popcount; lane j of each wave
-  // records slot j's count and the (slot, wave) table is scanned once; tab[wave][j] is
-  // then the number of flagged elements before this wave's part of slot j.
-  auto slot_offsets = [&](uint32_t bits) {
-    uint32_t mine = 0u;
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const uint32_t c = __popcll(__ballot((bits >> j) & 1u));
-      mine = lane == j ? c : mine;
-    }
-    __syncthreads();   // earlier readers of the table are done
-    if (lane < RPT) tab[wave][lane] = mine;
-    __syncthreads();
-    if (wave == 0) scan_slots(tab, lane);
-    __syncthreads();
-  };
-  const uint64_t below = (1ull << lane) - 1ull;
-  uint32_t eq_bits = 0u, take_bits = 0u;
+  uint64_t eq = 0u, take = 0u;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    eq_bits |= uint32_t(j < jmax && key[j] == T) << j;
-    take_bits |= uint32_t(j < jmax && key[j] > T) << j;
+    eq |= uint64_t(key[j] == T) << j;
+    take |= uint64_t(key[j] > T) << j;
   }
-  // slots go in groups of four (one wide table read each); the fences keep the compiler
-  // from hoisting every group's reads and ballots at once
+  uint32_t base[RCH];
   if (all_ties) {
-    take_bits |= eq_bits;
+    take |= eq;
   } else {
-    slot_offsets(eq_bits);
+    // ties ranked in index order; the first rem are kept
+    chunk_offsets(eq, base, wtot[0], lane, wave);
 #pragma unroll
-    for (int q = 0; q < RPT / 4; ++q) {
-      const uint4 o = *reinterpret_cast<const uint4*>(&tab[wave][4 * q]);
-      const uint32_t ov[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int j = 4 * q + e;
-        const uint32_t rank = ov[e] + __popcll(__ballot((eq_bits >> j) & 1u) & below);
-        take_bits |= uint32_t(((eq_bits >> j) & 1u) && rank < rem) << j;
-      }
-      __builtin_amdgcn_sched_barrier(0);
+    for (int j = 0; j < RPT; ++j) {
+      const uint32_t below = uint32_t(__popcll(eq & (((1ull << (j & 3)) - 1ull) << (j & ~3))));
+      take |= uint64_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
     }
   }
-  slot_offsets(take_bits);
+  chunk_offsets(take, base, wtot[1], lane, wave);
+  int t4s = 4 * tid;
+  asm volatile("" : "+v"(t4s));
 #pragma unroll
-  for (int q = 0; q < RPT / 4; ++q) {
-    const uint4 o = *reinterpret_cast<const uint4*>(&tab[wave][4 * q]);
-    const uint32_t ov[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = 4 * q + e;
-      const uint32_t pos = ov[e] + __popcll(__ballot((take_bits >> j) & 1u) & below);
-      if (((take_bits >> j) & 1u) && pos < uint32_t(k))   // pos < k always; bounds the store
-        out[pos] = j * RNT + tid;
-    }
+  for (int j = 0; j < RPT; ++j) {
+    const uint32_t pos =
+        base[j >> 2] + uint32_t(__popcll(take & (((1ull << (j & 3)) - 1ull) << (j & ~3))));
+    if (((take >> j) & 1u) && pos < uint32_t(k))   // pos < k always; bounds the store
+      out[pos] = (j >> 2) * RCHUNK + t4s + (j & 3);
     __builtin_amdgcn_sched_barrier(0);
   }
 }

@@ -91,6 +91,46 @@ def test_select_score_ranges():
                                           err_msg=f"segment {i} k={k}")
 
 
+def test_select_register_path_branches():
+    """Segments of 8193..32768 scores (the register-resident kernel) built to take each of
+    its branches: +inf keys that fill the budget or only part of it, a threshold bucket
+    too full for the candidate list (a narrow band inside a wide range), a range of fewer
+    than 256 key units, every finite score equal, and the four-load read (start not
+    16-byte aligned, length not divisible by four)."""
+    r = np.random.default_rng(77)
+    n = 32768
+    base = np.float32(11.0)
+    half_inf = r.exponential(3.0, n).astype(np.float32)
+    half_inf[r.permutation(n)[: n // 2]] = np.inf
+    some_inf = r.exponential(3.0, n).astype(np.float32)
+    some_inf[r.integers(0, n, 100)] = np.inf
+    some_inf[-1] = np.inf
+    band = (base + r.uniform(0.0, 1e-4, n)).astype(np.float32)
+    band[r.permutation(n)[:2768]] = r.uniform(0.0, 100.0, 2768).astype(np.float32)
+    ulps = (np.float32(1.0) + r.integers(0, 200, n).astype(np.float32) * np.float32(2.0 ** -23))
+    ulps = ulps.astype(np.float32)
+    flat = np.full(n, np.log(128256.0), dtype=np.float32)
+    flat[::97] = np.inf
+    segs = [half_inf, some_inf, band, ulps, flat]
+    s = np.concatenate(segs).astype(np.float32)
+    starts = [i * n for i in range(len(segs))]
+    for k in (1, 100, 8192, n // 2 + 5, n - 1):
+        print(f"[select] register branches k={k}", flush=True)
+        got = _gpu_select(s, starts, [n] * len(segs), [k] * len(segs))
+        for i, st in enumerate(starts):
+            np.testing.assert_array_equal(got[i * k:(i + 1) * k], O.select_keep(s[st:st + n], k),
+                                          err_msg=f"segment {i} k={k}")
+    # unaligned start, odd length: the four-load read
+    m = 30001
+    t = np.concatenate([np.zeros(3, np.float32), some_inf[:m], band[:m]]).astype(np.float32)
+    for k in (7, 7500, m - 2):
+        print(f"[select] unaligned k={k}", flush=True)
+        got = _gpu_select(t, [3, 3 + m], [m, m], [k, k])
+        for i, st in enumerate([3, 3 + m]):
+            np.testing.assert_array_equal(got[i * k:(i + 1) * k], O.select_keep(t[st:st + m], k),
+                                          err_msg=f"unaligned segment {i} k={k}")
+
+
 def test_select_overlapping_segments_identical_lists():
     r = np.random.default_rng(9)
     s = r.standard_normal(4096).astype(np.float32)
