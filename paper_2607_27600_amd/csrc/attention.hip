@@ -310,6 +310,11 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     sn[0] = f32x16{};
     sn[1] = f32x16{};
     __builtin_amdgcn_sched_barrier(0);
+    // The section that carries the exponentials issues at raised wave priority, so that on a
+    // SIMD shared with a wave in another section its MFMAs and exponentials go first
+    // (measured: 4-7% faster at n = 4096, 1.5% at 32768; the same priority over both
+    // sections, or over the P V section, gains less or nothing).
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (j + 3 < 16) kf[(j + 3) & 3] = kfrag(Kn, j + 3);
@@ -339,6 +344,7 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     vf[0] = vfrag(Vc, 0);
     vf[1] = vfrag(Vc, 1);
     vf[2] = vfrag(Vc, 2);
+    __builtin_amdgcn_s_setprio(0);
     pack(0);
     float ls0 = 0.f, ls1 = 0.f, m0 = -INFINITY, m1 = -INFINITY;
     __builtin_amdgcn_sched_barrier(0);
