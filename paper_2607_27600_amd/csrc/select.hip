@@ -201,13 +201,14 @@ __device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int
 // Ranks in index order of the keys flagged in m (bit 4c + i: slot i of chunk c): base[c]
 // = flagged keys before this thread's part of chunk c.  wtot: [RWAVES][RCH / 2] words of
 // LDS owned by this call.  Contains one barrier.
-__device__ __forceinline__ void chunk_offsets(uint64_t m, uint32_t (&base)[RCH],
+static_assert(RPT == 32, "one bit per key in a 32-bit mask");
+__device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
                                               uint32_t (*wtot)[RCH / 2], int lane, int wave) {
   uint32_t own[RCH / 2], inc[RCH / 2];
 #pragma unroll
   for (int q = 0; q < RCH / 2; ++q) {
-    own[q] = uint32_t(__popcll((m >> (8 * q)) & 0xfull)) |
-             (uint32_t(__popcll((m >> (8 * q + 4)) & 0xfull)) << 16);
+    own[q] = uint32_t(__popc((m >> (8 * q)) & 0xfu)) |
+             (uint32_t(__popc((m >> (8 * q + 4)) & 0xfu)) << 16);
     inc[q] = own[q];
   }
   // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
@@ -290,12 +291,12 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
   // the compiler recomputes it instead of keeping 64 indices (and their compare masks)
   // live across the kernel.  vbits: bit j set when key j lies inside the segment.
   asm volatile("" : "+v"(t4));
-  uint64_t vbits = 0u;
+  uint32_t vbits = 0u;
 #pragma unroll
   for (int c = 0; c < RCH; ++c) {
     // slots i < n - (c * RCHUNK + 4 tid) of chunk c hold scores
     const int nv = min(max(n - c * RCHUNK - t4, 0), RCW);
-    vbits |= uint64_t((1u << nv) - 1u) << (RCW * c);
+    vbits |= ((1u << nv) - 1u) << (RCW * c);
   }
   auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
 
@@ -397,9 +398,10 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
           // low hi bits, each thread's after those of the lanes before it.
           const int L = hi;
           const uint32_t lmask = (1u << L) - 1u;
-          uint32_t mine = 0u;
+          uint32_t cmask = 0u;
 #pragma unroll
-          for (int j = 0; j < RPT; ++j) mine += uint32_t(key[j] != rinf && (key[j] >> L) == prefix);
+          for (int j = 0; j < RPT; ++j) cmask |= uint32_t(key[j] != rinf && (key[j] >> L) == prefix) << j;
+          const uint32_t mine = uint32_t(__popc(cmask));
           uint32_t incl = mine;
 #pragma unroll
           for (int off = 1; off < 64; off <<= 1) {
@@ -411,9 +413,8 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
           uint32_t pos = uint32_t(__shfl(int(base), 63)) + incl - mine;
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
-            const uint32_t rel = key[j];
-            if (rel != rinf && (rel >> L) == prefix) {
-              if (pos < uint32_t(CMAX)) cand[pos] = rel & lmask;
+            if ((cmask >> j) & 1u) {
+              if (pos < uint32_t(CMAX)) cand[pos] = key[j] & lmask;
               ++pos;
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -432,9 +433,16 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
 #pragma unroll
               for (int q = 0; q < 4; ++q) whist[4 * lane + q] = 0u;
               asm volatile("" ::: "memory");
-              for (int i = lane; i < nc; i += 64) {
-                const uint32_t v = cand[i];
-                if ((v >> h2) == p2) atomicAdd(&whist[(v >> l2) & m2], 1u);
+              // eight reads in flight before their atomics: the list is walked at LDS
+              // throughput rather than one read latency per element
+              for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
+                uint32_t vv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) vv[u] = cand[min(i0 + u * 64 + lane, CMAX - 1)];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                  if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
+                    atomicAdd(&whist[(vv[u] >> l2) & m2], 1u);
               }
               __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
               asm volatile("" ::: "memory");
@@ -467,11 +475,11 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
   // includes padding cannot: real ties alone already reach rem)
   const bool all_ties = cnt == rem;
 
-  uint64_t eq = 0u, take = 0u;
+  uint32_t eq = 0u, take = 0u;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
-    eq |= uint64_t(key[j] == T) << j;
-    take |= uint64_t(key[j] > T) << j;
+    eq |= uint32_t(key[j] == T) << j;
+    take |= uint32_t(key[j] > T) << j;
   }
   uint32_t base[RCH];
   if (all_ties) {
@@ -481,19 +489,29 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
     chunk_offsets(eq, base, wtot[0], lane, wave);
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
-      const uint32_t below = uint32_t(__popcll(eq & (((1ull << (j & 3)) - 1ull) << (j & ~3))));
-      take |= uint64_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
+      const uint32_t below = uint32_t(__popc(eq & (((1u << (j & 3)) - 1u) << (j & ~3))));
+      take |= uint32_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
     }
   }
   chunk_offsets(take, base, wtot[1], lane, wave);
   int t4s = 4 * tid;
   asm volatile("" : "+v"(t4s));
+  // A thread's kept keys of chunk c take consecutive ranks base[c], base[c] + 1, ...;
+  // store u writes each lane's u-th kept key of the chunk (consecutive lanes write mostly
+  // consecutive ranks), and is skipped when no lane of the wave has one.
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    const uint32_t pos =
-        base[j >> 2] + uint32_t(__popcll(take & (((1ull << (j & 3)) - 1ull) << (j & ~3))));
-    if (((take >> j) & 1u) && pos < uint32_t(k))   // pos < k always; bounds the store
-      out[pos] = (j >> 2) * RCHUNK + t4s + (j & 3);
+  for (int c = 0; c < RCH; ++c) {
+    uint32_t t = (take >> (RCW * c)) & 0xfu;
+#pragma unroll
+    for (int u = 0; u < RCW; ++u) {
+      if (!__any(t != 0u)) break;
+      if (t != 0u) {
+        const uint32_t pos = base[c] + uint32_t(u);
+        if (pos < uint32_t(k))   // pos < k always; bounds the store
+          out[pos] = c * RCHUNK + t4s + __builtin_ctz(t);
+        t &= t - 1u;
+      }
+    }
     __builtin_amdgcn_sched_barrier(0);
   }
 }
