@@ -119,7 +119,7 @@ typedef struct cc_problem {
   const int32_t* cu_seqlens_d; /* the same values in device memory */
   int32_t n_heads_q;
   int32_t n_heads_kv;          /* divides n_heads_q */
-  int32_t head_dim;            /* 64 or 128 */
+  int32_t head_dim;            /* fp32: 64 or 128; bf16: 128 */
   int32_t hidden;              /* D: model width, rows of W_o */
   int32_t vocab;               /* V: rows of the LM head */
   int32_t n_layers;            /* FULL only: transformer layers (<= kv.n_layers) */
