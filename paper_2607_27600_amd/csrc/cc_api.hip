@@ -173,7 +173,7 @@ struct ScoreLayout {
 };
 
 struct FullLayout {
-  size_t attn, rot, h, a, q, o, act, lm, total;
+  size_t attn, rot, h, a, q, o, act, lm, part, total;
 };
 
 FullLayout full_layout(const cc_problem* p) {
@@ -197,6 +197,18 @@ FullLayout full_layout(const cc_problem* p) {
   off += align_up(N * size_t(p->ffn) * 2);
   L.lm = off;
   off += lmhead_ws_bytes(p);
+  // split-K partial sums of the projections whose tiles underfill the chip (small N)
+  const int D = p->hidden, F = p->ffn, hd = int(HD);
+  size_t part = 0;
+  auto need = [&](int M, int Nn, int K) {
+    const int S = gemm_split_slices(M, Nn, K);
+    if (S > 1) part = std::max(part, size_t(S) * size_t(M) * size_t(Nn) * sizeof(float));
+  };
+  need(hd, int(N), D);   // W_q
+  need(int(N), D, hd);   // W_o
+  need(int(N), D, F);    // W_down
+  L.part = off;
+  off += align_up(part);
   L.total = off;
   return L;
 }
@@ -325,18 +337,19 @@ cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, vo
   void* q = at(ws, L.q);
   void* o = at(ws, L.o);
   void* act = at(ws, L.act);
+  float* part = reinterpret_cast<float*>(at(ws, L.part));
   CC_HIP(launch_rope_table(in->pos_ids, p->cu_seqlens_d, p->n_seqs, rot, N, p->head_dim,
                            double(p->rope_theta), s));
   CC_HIP(launch_embed(in->embed, in->token_ids, h, N, D, s));
   for (int l = 0; l < p->n_layers; ++l) {
     const cc_layer_weights& W = in->layers_h[l];
     CC_HIP(launch_rmsnorm(h, W.attn_norm, a, N, D, p->rms_eps, s));
-    CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, s));
+    CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, part, s));
     CC_TRY(run_attention(p, q, &in->kv, l, o, at(ws, L.attn), s, l == 0));
-    CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, s));
+    CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, part, s));
     CC_HIP(launch_rmsnorm(h, W.mlp_norm, a, N, D, p->rms_eps, s));
     CC_HIP(launch_gate_up_swiglu(W.w_gate, W.w_up, a, act, N, D, F, s));
-    CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
+    CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, part, s));
   }
   CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
   return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, 0,
@@ -373,17 +386,18 @@ cc_status score_last_h(const cc_problem* p, const cc_inputs* in, float* scores, 
   void* q = at(ws, L.q);
   void* o = at(ws, L.o);
   void* act = at(ws, L.act);
+  float* part = reinterpret_cast<float*>(at(ws, L.part));
   const cc_layer_weights& W = in->layers_h[0];
   CC_HIP(launch_rope_table(in->pos_ids, p->cu_seqlens_d, p->n_seqs, rot, N, p->head_dim,
                            double(p->rope_theta), s));
   CC_HIP(launch_embed(in->h_last, nullptr, h, N, D, s));   // widen H to the fp32 stream
   CC_HIP(launch_rmsnorm(h, W.attn_norm, a, N, D, p->rms_eps, s));
-  CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, s));
+  CC_HIP(launch_qproj_rope(W.wq, a, q, rot, N, D, HD, part, s));
   CC_TRY(run_attention(p, q, &in->kv, in->kv.n_layers - 1, o, at(ws, L.attn), s));
-  CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, s));
+  CC_HIP(launch_linear_residual(o, W.wo, h, N, D, HD, part, s));
   CC_HIP(launch_rmsnorm(h, W.mlp_norm, a, N, D, p->rms_eps, s));
   CC_HIP(launch_gate_up_swiglu(W.w_gate, W.w_up, a, act, N, D, F, s));
-  CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, s));
+  CC_HIP(launch_linear_residual(act, W.w_down, h, N, D, F, part, s));
   CC_HIP(launch_rmsnorm(h, in->final_norm, a, N, D, p->rms_eps, s));
   return run_lmhead(p, a, in->w_lm, in->token_ids, scores, nullptr, at(ws, L.lm), s, 0,
                     in->w_lm_packed);

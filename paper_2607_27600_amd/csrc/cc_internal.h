@@ -188,12 +188,18 @@ struct CompactLaunch {
 hipError_t launch_compact(const CompactLaunch& a, hipStream_t s);
 
 // FULL-mode building blocks (bf16, head_dim 128).
+// Split-K: slices a [M][K] x [N][K] product is cut into along K when its 256 x 256 tiles
+// would fill under half the chip (1: one pass).  A split product needs a workspace of
+// slices * M * N floats for its partial sums.
+int gemm_split_slices(int M, int N, int K);
 // q[n][:] = RoPE(W_q a[n]) with rot[n][e] = (cos, sin) of the entry's rotation angle.
+// part: gemm_split_slices(HD, N, D) * N * HD floats when that count exceeds 1, else unused.
 hipError_t launch_qproj_rope(const void* wq, const void* a, void* q, const float2* rot, int N,
-                             int D, int HD, hipStream_t s);
+                             int D, int HD, float* part, hipStream_t s);
 // h[m][:] += x[m][:] W^T (fp32 residual stream).
+// part: gemm_split_slices(M, N, K) * M * N floats when that count exceeds 1, else unused.
 hipError_t launch_linear_residual(const void* x, const void* w, float* h, int M, int N, int K,
-                                  hipStream_t s);
+                                  float* part, hipStream_t s);
 // act[n][f] = silu(W_gate b[n])[f] * (W_up b[n])[f].
 hipError_t launch_gate_up_swiglu(const void* w_gate, const void* w_up, const void* b, void* act,
                                  int N, int D, int F, hipStream_t s);

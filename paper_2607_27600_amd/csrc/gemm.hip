@@ -15,6 +15,7 @@
 // in-lane.  Tiles are rasterised entry-tile-fastest so consecutive workgroups share one
 // LM-head tile.
 // fp32 kernel: a plain LDS-tiled FMA GEMM with the same two epilogues.
+#include <algorithm>
 #include <type_traits>
 
 #include "cc_internal.h"
@@ -36,6 +37,7 @@ struct GemmArgs {
   int64_t lda, ldb;
   int tiles_m, tiles_n;
   const u16* A2;   // gated loader: logical A rows alternate in blocks of 32 between A and A2
+  int kt_split = 0;   // split-K: k-tiles per slice, slice = blockIdx.y (0: one pass over K)
 };
 
 __device__ __forceinline__ uint4 ld16(const u16* p) { return *reinterpret_cast<const uint4*>(p); }
@@ -227,6 +229,87 @@ struct EpiResidual {
   }
 };
 
+// Split-K: one K slice's fp32 products, part[slice][m][n] (NM = false, the layout of the
+// residual stream) or part[slice][n][m] (NM = true, the token-major layout of the query
+// projection).  A reduce kernel sums the slices in order and applies the real epilogue.
+template <bool NM>
+struct EpiPartial {
+  float* part;
+  __device__ void operator()(const f32x16 (&acc)[GMB][GNB], const GemmArgs& g, int tm, int m0w,
+                             int n0w, int lane, u16* lds) const {
+    (void)tm;
+    (void)lds;
+    const int hi = lane >> 5, col = lane & 31;
+    float* p = part + int64_t(blockIdx.y) * g.M * g.N;
+#pragma unroll
+    for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int n = n0w + nb * 32 + col;
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int m = m0w + mb * 32 + e4 * 8 + hi * 4;   // rows m .. m+3 of this lane
+          if constexpr (NM) {
+            // M is a multiple of 4 here (whole heads), so the four rows go out as one float4
+            if (m < g.M)
+              *reinterpret_cast<float4*>(p + int64_t(n) * g.M + m) =
+                  make_float4(acc[mb][nb][4 * e4], acc[mb][nb][4 * e4 + 1],
+                              acc[mb][nb][4 * e4 + 2], acc[mb][nb][4 * e4 + 3]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (m + i < g.M) p[int64_t(m + i) * g.N + n] = acc[mb][nb][4 * e4 + i];
+          }
+        }
+      }
+  }
+};
+
+// Split-K sum into the fp32 residual stream: h[i] += part[0][i] + ... + part[S-1][i]
+// (count a multiple of 4).
+__global__ __launch_bounds__(256) void reduce_residual(const float* __restrict__ part, int S,
+                                                       int64_t count, float* __restrict__ h) {
+  const int64_t i = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (i >= count) return;
+  float4 t = *reinterpret_cast<const float4*>(part + i);
+  for (int sl = 1; sl < S; ++sl) {
+    const float4 v = *reinterpret_cast<const float4*>(part + int64_t(sl) * count + i);
+    t.x += v.x;
+    t.y += v.y;
+    t.z += v.z;
+    t.w += v.w;
+  }
+  float4 r = *reinterpret_cast<const float4*>(h + i);
+  r.x += t.x;
+  r.y += t.y;
+  r.z += t.z;
+  r.w += t.w;
+  *reinterpret_cast<float4*>(h + i) = r;
+}
+
+// Split-K query projection: q = the sum of the slices (part [S][N][M]), then the rotate-half
+// rotary embedding of EpiRope at each entry's position, stored as bf16 [N][M].  One thread
+// per (entry, head, pair e of 0..63); head_dim 128.
+__global__ __launch_bounds__(256) void reduce_rope(const float* __restrict__ part, int S, int N,
+                                                   int M, const float2* __restrict__ rot,
+                                                   u16* __restrict__ q) {
+  const int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int half = M / 2;
+  if (t >= int64_t(N) * half) return;
+  const int n = int(t / half), r = int(t % half);
+  const int e = r & 63, m = (r >> 6) * 128 + e;
+  const int64_t cnt = int64_t(N) * M, o = int64_t(n) * M + m;
+  float a = part[o], b = part[o + 64];
+  for (int sl = 1; sl < S; ++sl) {
+    a += part[sl * cnt + o];
+    b += part[sl * cnt + o + 64];
+  }
+  const float2 cs = rot[int64_t(n) * 64 + e];
+  q[o] = f2bf(a * cs.x - b * cs.y);
+  q[o + 64] = f2bf(b * cs.x + a * cs.y);
+}
+
 // M = interleaved gate/up rows (see the gated loader), N = entries:
 // act[n][f] = silu(gate) * up, bf16, token-major [N][F].
 struct EpiSwiglu {
@@ -328,6 +411,9 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int hi = lane >> 5, col = lane & 31;
   const int wm = wave / WGN, wn = wave % WGN;
+  // split-K: this workgroup's slice covers k-tiles kt0 .. kt0 + nk - 1
+  const int kt0 = g.kt_split ? int(blockIdx.y) * g.kt_split : 0;
+  const int nk = g.kt_split ? min(g.kt_split, g.K / GBK - kt0) : g.K / GBK;
 
   // wave w, load instruction j covers tile rows (8w + j) * 8 .. +8; rows past the matrix
   // edge are clamped to the last row (their products land in outputs the epilogues
@@ -343,11 +429,11 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
       // rows [64i, 64i+32) are W_gate rows [32i, 32i+32), rows [64i+32, 64i+64) the same
       // W_up rows, so each wave's 32-row MFMA blocks pair gate and up for one column range
       const u16* base = ((ra >> 5) & 1) ? g.A2 : g.A;
-      ga[j] = base + int64_t((ra >> 6) * 32 + (ra & 31)) * g.lda + c * 8;
+      ga[j] = base + int64_t((ra >> 6) * 32 + (ra & 31)) * g.lda + c * 8 + kt0 * GBK;
     } else {
-      ga[j] = g.A + int64_t(ra) * g.lda + c * 8;
+      ga[j] = g.A + int64_t(ra) * g.lda + c * 8 + kt0 * GBK;
     }
-    gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8;
+    gb[j] = g.B + int64_t(min(n0 + r, g.N - 1)) * g.ldb + c * 8 + kt0 * GBK;
   }
   // Half h of a stage: h = 0 the A rows, h = 1 the B rows (LPW direct loads per wave).
   auto issue_half = [&](u16* stage, int k0, int h) {
@@ -402,7 +488,6 @@ __global__ __launch_bounds__(GNT, 1) void gemm_tn_bf16(GemmArgs g, Epi epi) {
     }
     __builtin_amdgcn_sched_barrier(0);
   };
-  const int nk = g.K / GBK;
   bf16x8 fa0[GMB], fb0[GNB], fa1[GMB], fb1[GNB];
   // One k-tile from `cur`; fragments of each step are read during the previous step.  The
   // loads of a stage are split in two halves issued between MFMAs, never in one burst: when
@@ -1351,19 +1436,63 @@ GemmArgs make_args(const void* a, const void* b, int M, int N, int K, int64_t ld
 }
 }  // namespace
 
+int gemm_split_slices(int M, int N, int K) {
+  const int tiles = ((M + GBM - 1) / GBM) * ((N + GBN - 1) / GBN);
+  const int nk = K / GBK;
+  if (tiles >= 128 || nk < 8) return 1;
+  // enough slices to give every CU a workgroup, at least four k-tiles per slice, at most 8
+  const int want = std::max(1, std::min({(256 + tiles - 1) / tiles, nk / 4, 8}));
+  const int per = (nk + want - 1) / want;
+  return (nk + per - 1) / per;
+}
+
+namespace {
+// k-tiles per slice for the slice count gemm_split_slices chose
+int split_ktiles(int K, int S) {
+  const int nk = K / GBK;
+  return (nk + S - 1) / S;
+}
+}  // namespace
+
 hipError_t launch_qproj_rope(const void* wq, const void* a, void* q, const float2* rot, int N,
-                             int D, int HD, hipStream_t s) {
+                             int D, int HD, float* part, hipStream_t s) {
   if (N == 0) return hipSuccess;
   GemmArgs g = make_args(wq, a, HD, N, D, D, D);
+  const int S = gemm_split_slices(HD, N, D);
+  if (S > 1) {
+    g.kt_split = split_ktiles(D, S);
+    EpiPartial<true> e{part};
+    hipLaunchKernelGGL(gemm_tn_bf16<EpiPartial<true>>, dim3(g.tiles_m * g.tiles_n, S), dim3(GNT),
+                       0, s, g, e);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const int64_t threads = int64_t(N) * (HD / 2);
+    hipLaunchKernelGGL(reduce_rope, dim3(unsigned((threads + 255) / 256)), dim3(256), 0, s, part,
+                       S, N, HD, rot, static_cast<u16*>(q));
+    return hipGetLastError();
+  }
   EpiRope e{static_cast<u16*>(q), rot};
   hipLaunchKernelGGL(gemm_tn_bf16<EpiRope>, dim3(g.tiles_m * g.tiles_n), dim3(GNT), 0, s, g, e);
   return hipGetLastError();
 }
 
 hipError_t launch_linear_residual(const void* x, const void* w, float* h, int M, int N, int K,
-                                  hipStream_t s) {
+                                  float* part, hipStream_t s) {
   if (M == 0) return hipSuccess;
   GemmArgs g = make_args(x, w, M, N, K, K, K);
+  const int S = gemm_split_slices(M, N, K);
+  if (S > 1) {
+    g.kt_split = split_ktiles(K, S);
+    EpiPartial<false> e{part};
+    hipLaunchKernelGGL(gemm_tn_bf16<EpiPartial<false>>, dim3(g.tiles_m * g.tiles_n, S),
+                       dim3(GNT), 0, s, g, e);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const int64_t count = int64_t(M) * N;
+    hipLaunchKernelGGL(reduce_residual, dim3(unsigned((count / 4 + 255) / 256)), dim3(256), 0, s,
+                       part, S, count, h);
+    return hipGetLastError();
+  }
   EpiResidual e{h};
   hipLaunchKernelGGL(gemm_tn_bf16<EpiResidual>, dim3(g.tiles_m * g.tiles_n), dim3(GNT), 0, s, g,
                      e);
