@@ -1154,9 +1154,10 @@ __global__ __launch_bounds__(256) void target_logit(const T* __restrict__ u,
 }
 
 // One workgroup per 16 entries: thread (group gi, entry e) folds the vocabulary tiles
-// gi, gi+16, ... of entry e (16 consecutive entries read 128 contiguous bytes of a tile's
-// row of partials), then the 16 groups are folded in LDS.
-constexpr int CMB_E = 16, CMB_G = 16;
+// gi, gi+64, ... of entry e (16 consecutive entries read 128 contiguous bytes of a tile's
+// row of partials; up to 512 tiles are eight loads per thread, all in flight at once), then
+// the 64 groups are folded by shuffles within each wave and across the waves in LDS.
+constexpr int CMB_E = 16, CMB_G = 64;
 
 __device__ __forceinline__ void lse_fold(float& M, float& S, float m, float s) {
   if (m == -INFINITY) return;
@@ -1172,31 +1173,38 @@ __global__ __launch_bounds__(CMB_E * CMB_G) void lse_combine(const float2* parti
                                                             const float* target, const int32_t* cu,
                                                             int n_seqs, int n_frozen, int N,
                                                             float* scores, float* lse_out) {
-  __shared__ float2 red[CMB_G][CMB_E];
+  __shared__ float2 red[CMB_E * CMB_G / 64][CMB_E];
   const int e = threadIdx.x % CMB_E, gi = threadIdx.x / CMB_E;
   const int n = blockIdx.x * CMB_E + e;
   float M = -INFINITY, S = 0.f;
   if (n < N) {
-    // eight independent loads in flight per thread, then fold
-    int t = gi;
-    for (; t + 7 * CMB_G < n_tiles; t += 8 * CMB_G) {
+    // eight independent loads in flight per thread (tiles past the end fold as empty)
+    for (int t0 = gi; t0 < n_tiles; t0 += 8 * CMB_G) {
       float2 p[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) p[q] = partial[int64_t(t + q * CMB_G) * N + n];
+      for (int q = 0; q < 8; ++q) {
+        const int t = t0 + q * CMB_G;
+        p[q] = t < n_tiles ? partial[int64_t(t) * N + n] : make_float2(-INFINITY, 0.f);
+      }
 #pragma unroll
       for (int q = 0; q < 8; ++q) lse_fold(M, S, p[q].x, p[q].y);
     }
-    for (; t < n_tiles; t += CMB_G) {
-      const float2 p = partial[int64_t(t) * N + n];
-      lse_fold(M, S, p.x, p.y);
-    }
   }
-  red[gi][e] = make_float2(M, S);
+  // the four groups of an entry within a wave (lanes e, e+16, e+32, e+48) fold by
+  // shuffles, then the waves' results through LDS
+#pragma unroll
+  for (int off = 16; off < 64; off <<= 1) {
+    const float m2 = __shfl_xor(M, off), s2 = __shfl_xor(S, off);
+    lse_fold(M, S, m2, s2);
+  }
+  constexpr int NWV = CMB_E * CMB_G / 64;
+  const int wv = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) < CMB_E) red[wv][e] = make_float2(M, S);
   __syncthreads();
   if (gi == 0 && n < N) {
     float Mt = -INFINITY, St = 0.f;
 #pragma unroll
-    for (int r = 0; r < CMB_G; ++r) lse_fold(Mt, St, red[r][e].x, red[r][e].y);
+    for (int r = 0; r < NWV; ++r) lse_fold(Mt, St, red[r][e].x, red[r][e].y);
     const float lse = Mt + logf(St);
     // sequence of entry n: the last b with cu[b] <= n
     int lo = 0, hi = n_seqs - 1;
