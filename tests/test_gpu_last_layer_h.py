@@ -62,12 +62,13 @@ def test_small_ragged_all_rows_with_gains_and_positions():
 
 def test_split_k_projections_all_rows():
     """Shapes whose projections are cut along K (their 256 x 256 tiles fill under half the
-    chip): W_q in 4 slices (hidden 1024), W_o in 4, W_down in 8 with a short last slice
-    (ffn 2880 = 45 k-tiles of 64), against the oracle on every row."""
+    chip): W_q in 4 slices (hidden 1024), W_o in 4, W_down in 5 with a short last slice
+    (ffn 2944 = 46 k-tiles of 64: four slices of 10 and one of 6), against the oracle on
+    every row."""
     from paper_2607_27600_amd import cc
     from paper_2607_27600_amd.workload import Workload
     cfg = C.shrink(C.C2H, seq_lens=(300, 45), n_heads_q=8, n_heads_kv=2, hidden=1024,
-                   ffn=2880, vocab=1000, cache_layers=1, keep=(75, 11))
+                   ffn=2944, vocab=1000, cache_layers=1, keep=(75, 11))
     print(f"[last_layer_h] split-K lens={cfg.seq_lens} D={cfg.hidden} F={cfg.ffn}", flush=True)
     w = Workload(cfg, keep_host=True)
     scores = torch.full((cfg.n_tokens,), float("nan"), device="cuda")
