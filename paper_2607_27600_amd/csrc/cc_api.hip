@@ -787,13 +787,15 @@ cc_status cc_compact_kv(const cc_problem* p, const cc_kv* kv, const int32_t* kee
   if (plan.total != compact_ws_bytes_for(p, per_head, L)) return CC_ERR_ARG;
   CC_TRY(check_ws(ws, ws_bytes, plan.total));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  CC_HIP(hipMemcpyAsync(at(ws, plan.off_lists), plan.lists.data(),
-                        plan.lists.size() * sizeof(CompactList), hipMemcpyHostToDevice, s));
+  // the three tables go up as one host image of the workspace prefix: one copy, not three
+  // (each copy from pageable memory is a separate transfer on the stream)
+  std::vector<char> img(plan.off_seq + plan.seq_list.size() * sizeof(int32_t));
+  std::memcpy(img.data() + plan.off_lists, plan.lists.data(), plan.lists.size() * sizeof(CompactList));
   if (!plan.planes.empty())
-    CC_HIP(hipMemcpyAsync(at(ws, plan.off_planes), plan.planes.data(),
-                          plan.planes.size() * sizeof(CompactPlane), hipMemcpyHostToDevice, s));
-  CC_HIP(hipMemcpyAsync(at(ws, plan.off_seq), plan.seq_list.data(),
-                        plan.seq_list.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
+    std::memcpy(img.data() + plan.off_planes, plan.planes.data(),
+                plan.planes.size() * sizeof(CompactPlane));
+  std::memcpy(img.data() + plan.off_seq, plan.seq_list.data(), plan.seq_list.size() * sizeof(int32_t));
+  CC_HIP(hipMemcpyAsync(ws, img.data(), img.size(), hipMemcpyHostToDevice, s));
   CompactLaunch c;
   c.n_tensors = 2;
   const cc_kv* dst = out ? out : kv;
@@ -882,10 +884,11 @@ cc_status cc_compact_rows(const cc_problem* p, void* rows, int32_t row_bytes,
   CC_TRY(check_ws(ws, ws_bytes, rows_ws_bytes(p, row_bytes)));
   if (planes.empty()) return CC_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  CC_HIP(hipMemcpyAsync(ws, lists.data(), lists.size() * sizeof(CompactList),
-                        hipMemcpyHostToDevice, s));
-  CC_HIP(hipMemcpyAsync(at(ws, off_planes), planes.data(), planes.size() * sizeof(CompactPlane),
-                        hipMemcpyHostToDevice, s));
+  // both tables as one host image of the workspace prefix (one copy)
+  std::vector<char> img(off_planes + planes.size() * sizeof(CompactPlane));
+  std::memcpy(img.data(), lists.data(), lists.size() * sizeof(CompactList));
+  std::memcpy(img.data() + off_planes, planes.data(), planes.size() * sizeof(CompactPlane));
+  CC_HIP(hipMemcpyAsync(ws, img.data(), img.size(), hipMemcpyHostToDevice, s));
   auto view = [&](void* base) {
     KvView v{};
     v.base = base;
