@@ -155,8 +155,16 @@ struct SelSeg {
   int32_t k;
   int64_t out;     // keep_idx offset
 };
-hipError_t launch_select(const float* scores, const SelSeg* segs_d, int n_segs, int max_len,
-                         int32_t* keep, hipStream_t s);
+// Up to SEL_INLINE segment descriptors travel by value in the kernel arguments (no upload).
+constexpr int SEL_INLINE = 16;
+struct SelInline {
+  SelSeg s[SEL_INLINE];
+  int n;   // descriptors held here (0: all are read from the device table)
+};
+// segs_h: the descriptors on the host; segs_d: the same in device memory, read only when
+// n_segs > SEL_INLINE (may be null otherwise).
+hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg* segs_d,
+                         int n_segs, int max_len, int32_t* keep, hipStream_t s);
 
 // KV compaction: one workgroup per (list, layer, head, tensor) plane.
 struct CompactPlane {

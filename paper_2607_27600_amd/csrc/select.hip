@@ -45,11 +45,12 @@ __device__ __forceinline__ int block_scan(bool flag, int* wsum, int& total) {
 
 __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restrict__ scores,
                                                           const SelSeg* __restrict__ segs,
+                                                          SelInline inl,
                                                           int32_t* __restrict__ keep) {
   __shared__ uint32_t hist[256];
   __shared__ int wsum[SWAVES];
   __shared__ uint32_t sh_digit, sh_rem, sh_cnt;
-  const SelSeg sg = segs[blockIdx.x];
+  const SelSeg sg = int(blockIdx.x) < inl.n ? inl.s[blockIdx.x] : segs[blockIdx.x];
   const float* s = scores + sg.start;
   int32_t* out = keep + sg.out;
   const int n = sg.len, k = sg.k;
@@ -243,6 +244,7 @@ __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
 
 __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restrict__ scores,
                                                            const SelSeg* __restrict__ segs,
+                                                           SelInline inl,
                                                            int32_t* __restrict__ keep) {
   __shared__ uint32_t hist[2][RWAVES][256];
   __shared__ uint32_t tot[256];
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
   __shared__ uint32_t red[3][RWAVES];
   __shared__ uint32_t wtot[2][RWAVES][RCH / 2];
   __shared__ uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
-  const SelSeg sg = segs[blockIdx.x];
+  const SelSeg sg = int(blockIdx.x) < inl.n ? inl.s[blockIdx.x] : segs[blockIdx.x];
   const int n = sg.len, k = sg.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int32_t* out = keep + sg.out;
@@ -518,16 +520,21 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
 
 }  // namespace
 
-hipError_t launch_select(const float* scores, const SelSeg* segs_d, int n_segs, int max_len,
-                         int32_t* keep, hipStream_t s) {
+hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg* segs_d,
+                         int n_segs, int max_len, int32_t* keep, hipStream_t s) {
   if (n_segs == 0) return hipSuccess;
+  SelInline inl{};
+  if (n_segs <= SEL_INLINE) {
+    for (int i = 0; i < n_segs; ++i) inl.s[i] = segs_h[i];
+    inl.n = n_segs;
+  }
   // The register path pays a fixed cost per segment (its passes and scans are a chain of
   // block-wide barriers) that the re-reading kernel does not; it wins once a segment is
   // long enough for the repeated reads to dominate.
   if (max_len > 8192 && max_len <= RMAX)
-    hipLaunchKernelGGL(select_keep_regs, dim3(n_segs), dim3(RNT), 0, s, scores, segs_d, keep);
+    hipLaunchKernelGGL(select_keep_regs, dim3(n_segs), dim3(RNT), 0, s, scores, segs_d, inl, keep);
   else
-    hipLaunchKernelGGL(select_keep_kernel, dim3(n_segs), dim3(SNT), 0, s, scores, segs_d, keep);
+    hipLaunchKernelGGL(select_keep_kernel, dim3(n_segs), dim3(SNT), 0, s, scores, segs_d, inl, keep);
   return hipGetLastError();
 }
 

@@ -131,6 +131,26 @@ def test_select_register_path_branches():
                                           err_msg=f"unaligned segment {i} k={k}")
 
 
+@pytest.mark.parametrize("long_seg", [False, True])
+def test_select_many_segments(long_seg):
+    """More segments than travel in the kernel arguments (16): the descriptors go through
+    the workspace table; both kernels (longest segment at most 8192, or up to 32768)."""
+    r = np.random.default_rng(31 + long_seg)
+    lens = [int(x) for x in r.integers(1, 3000, 40)]
+    if long_seg:
+        lens[17] = 20000
+    s = r.exponential(3.0, sum(lens)).astype(np.float32)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    ks = [int(r.integers(0, n + 1)) for n in lens]
+    print(f"[select] {len(lens)} segments, longest {max(lens)}", flush=True)
+    got = _gpu_select(s, starts, lens, ks)
+    off = 0
+    for st, n, k in zip(starts, lens, ks):
+        np.testing.assert_array_equal(got[off:off + k], O.select_keep(s[st:st + n], k),
+                                      err_msg=f"len={n} k={k}")
+        off += k
+
+
 def test_select_overlapping_segments_identical_lists():
     r = np.random.default_rng(9)
     s = r.standard_normal(4096).astype(np.float32)
