@@ -40,10 +40,10 @@ struct AttnArgs {
   const u16* q;
   u16* o;
   const int32_t* cu;
-  const int4* work;
+  const int4* work;   // null for one sequence: item i is (0, i % nkv, i / nkv)
   KvView k, v;
   int layer;
-  int hq, g;
+  int hq, g, nkv;
   float c2;        // scale * log2(e)
   int inclusive;
 };
@@ -83,7 +83,10 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) u16 vl0[TILE];
   __shared__ __attribute__((aligned(1024))) u16 vl1[TILE];
 
-  const int4 w = a.work[blockIdx.x];
+  // work item: from the table, or for one sequence from the block index (row blocks in
+  // increasing order, heaviest first, KV heads fastest: the table's order)
+  const int4 w = a.work ? a.work[blockIdx.x]
+                        : make_int4(0, int(blockIdx.x) % a.nkv, int(blockIdx.x) / a.nkv, 0);
   const int b = w.x, kvh = w.y, rb = w.z;
   const int seq0 = a.cu[b];
   const int n = a.cu[b + 1] - seq0;
@@ -428,10 +431,10 @@ struct AttnArgsF {
   const float* q;
   float* o;
   const int32_t* cu;
-  const int4* work;
+  const int4* work;   // null for one sequence: item i is (0, i % nkv, i / nkv)
   KvView k, v;
   int layer;
-  int hq, g;
+  int hq, g, nkv;
   float scale;
   int inclusive;
 };
@@ -440,7 +443,10 @@ template <int D, bool PAGED>
 __global__ __launch_bounds__(F_ROWS) void attn_cc_f32(AttnArgsF a) {
   __shared__ float Ks[F_BN][D + 1];
   __shared__ float Vs[F_BN][D + 1];
-  const int4 w = a.work[blockIdx.x];
+  // work item: from the table, or for one sequence from the block index (row blocks in
+  // increasing order, heaviest first, KV heads fastest: the table's order)
+  const int4 w = a.work ? a.work[blockIdx.x]
+                        : make_int4(0, int(blockIdx.x) % a.nkv, int(blockIdx.x) / a.nkv, 0);
   const int b = w.x, kvh = w.y, rb = w.z;
   const int seq0 = a.cu[b];
   const int n = a.cu[b + 1] - seq0;
@@ -514,6 +520,7 @@ void fill_common(Args& x, const AttnLaunch& a) {
   x.layer = a.layer;
   x.hq = a.n_heads_q;
   x.g = a.n_heads_q / a.n_heads_kv;
+  x.nkv = a.n_heads_kv;
   x.inclusive = a.inclusive;
 }
 

@@ -237,14 +237,16 @@ cc_status run_attention(const cc_problem* p, const void* q, const cc_kv* kv, int
                         void* ws, hipStream_t s, bool upload = true) {
   std::vector<int4> work = attention_work(p);
   if (work.empty()) return CC_OK;
-  if (upload)
+  // one sequence: the kernel derives each item from its block index, nothing is uploaded
+  const bool table = p->n_seqs > 1;
+  if (upload && table)
     CC_HIP(hipMemcpyAsync(ws, work.data(), work.size() * sizeof(int4), hipMemcpyHostToDevice, s));
   AttnLaunch a;
   a.dtype = p->dtype;
   a.q = q;
   a.o = o;
   a.cu_d = p->cu_seqlens_d;
-  a.work_d = static_cast<const int4*>(ws);
+  a.work_d = table ? static_cast<const int4*>(ws) : nullptr;
   a.n_work = int(work.size());
   a.k = make_view(kv, kv->k, 1);
   a.v = make_view(kv, kv->v, 1);

@@ -74,7 +74,7 @@ struct AttnLaunch {
   const void* q;        // [N][Hq][d]
   void* o;              // [N][Hq][d]
   const int32_t* cu_d;  // device cu_seqlens
-  const int4* work_d;   // device work list {seq, kv head, row block, 0}
+  const int4* work_d;   // device work list {seq, kv head, row block, 0}; null for one sequence
   int n_work;
   KvView k, v;
   bool paged;
