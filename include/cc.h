@@ -119,8 +119,8 @@ typedef struct cc_problem {
   const int32_t* cu_seqlens_d; /* the same values in device memory */
   int32_t n_heads_q;
   int32_t n_heads_kv;          /* divides n_heads_q */
-  int32_t head_dim;            /* fp32: 64 or 128; bf16: 128 */
-  int32_t hidden;              /* D: model width, rows of W_o */
+  int32_t head_dim;            /* 64 or 128 (FULL and LAST_LAYER_H: 128) */
+  int32_t hidden;              /* D: model width, rows of W_o (bf16: a multiple of 64) */
   int32_t vocab;               /* V: rows of the LM head */
   int32_t n_layers;            /* FULL only: transformer layers (<= kv.n_layers) */
   int32_t ffn;                 /* FULL, LAST_LAYER_H: SwiGLU width */
@@ -131,7 +131,8 @@ typedef struct cc_problem {
                                   slots that are never evicted (score +inf) */
   int32_t lmhead_packed;       /* bf16 only: 1 = the LM head reads the packed weight
                                   cc_inputs.w_lm_packed (cc_pack_lmhead) and packs its
-                                  input rows in the workspace; 0 = row-major w_lm only */
+                                  input rows in the workspace (cc_inputs.w_lm is then
+                                  not read and may be NULL); 0 = row-major w_lm */
 } cc_problem;
 
 /* Weights of one transformer layer (FULL, LAST_LAYER_H), device pointers in `dtype`. */
@@ -155,16 +156,16 @@ typedef struct cc_inputs {
                                   NULL -> 0..n_b-1 */
   const void* w_o;             /* LAST_LAYER: [D][Hq*d] */
   const void* w_lm;            /* [V][D] LM head; LAST_LAYER_FUSED: [V][Hq*d], the
-                                  product W_lm W_o */
+                                  product W_lm W_o.  Not read (may be NULL) when
+                                  lmhead_packed = 1 */
   const void* embed;           /* FULL: [V][D] token embeddings */
   const cc_layer_weights* layers_h; /* FULL: host array [n_layers]; LAST_LAYER_H:
                                   host array [1], the last layer's weights */
   const void* final_norm;      /* FULL, LAST_LAYER_H: [D] final RMSNorm gain */
   const void* h_last;          /* LAST_LAYER_H: [N][D] stored activations entering
                                   the last layer (dtype), token-major like ids */
-  const void* w_lm_packed;     /* lmhead_packed = 1: w_lm in the packed layout of
-                                  cc_pack_lmhead (w_lm is still read for the target
-                                  logits) */
+  const void* w_lm_packed;     /* lmhead_packed = 1: the LM head in the packed layout
+                                  of cc_pack_lmhead */
 } cc_inputs;
 
 /* Human-readable name of a status code (static string). */
@@ -204,7 +205,10 @@ cc_status cc_lmhead_workspace(const cc_problem* p, size_t* bytes);
 
 /* LM head, log-softmax and target gather (Eq. (5)): for hidden rows u [N][D]
  * (dtype), scores[i] = logsumexp(W_lm u_i) - (W_lm u_i)[ids[i]], with the
- * last-entry / frozen rule applied.  lse (nullable) receives logsumexp. */
+ * last-entry / frozen rule applied.  The target logit is taken from the same
+ * accumulators as the log-sum-exp, and a difference that rounding takes below zero is
+ * returned as 0 (-log P >= 0).  lse (nullable) receives logsumexp.  This is the
+ * log-probability sub-step: log P(x_i | future) = -scores[i] for every finite score. */
 cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
                           const int32_t* token_ids, float* scores, float* lse,
                           void* workspace, size_t workspace_bytes, void* stream);
@@ -272,13 +276,12 @@ cc_status cc_pack_lmhead(const void* x, int64_t rows, int32_t cols, void* out,
                          size_t out_bytes, void* stream);
 
 /* cc_lmhead_score with p->lmhead_packed = 1: w_packed is w_lm [V][D] packed by
- * cc_pack_lmhead; w_lm itself is read for the target logits only.  The result equals
+ * cc_pack_lmhead (the row-major weight is not needed).  The result equals
  * cc_lmhead_score up to fp32 summation order (the packed kernel accumulates in another
  * order on the 16x16x32 matrix-core shape).  Workspace: cc_lmhead_workspace(p). */
-cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_lm,
-                                 const void* w_packed, const int32_t* token_ids,
-                                 float* scores, float* lse, void* workspace,
-                                 size_t workspace_bytes, void* stream);
+cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_packed,
+                                 const int32_t* token_ids, float* scores, float* lse,
+                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ selection */
 

@@ -119,11 +119,17 @@ def logsumexp_rows(z: np.ndarray) -> np.ndarray:
     return m + np.log(np.exp(z - m[:, None]).sum(axis=1))
 
 
-def surprise(u, w_lm, ids) -> tuple:
-    """Returns (score, lse, z_target) per row: score = lse(z) - z[x] = -log P(x)."""
+def surprise(u, w_lm, ids, spread: bool = False) -> tuple:
+    """Returns (score, lse, z_target) per row: score = lse(z) - z[x] = -log P(x).
+
+    spread=True appends the standard deviation of z over the vocabulary per row.  It is
+    not part of the method: the parity tests use it to size the rounding error a score
+    can carry, since the score moves with its input u through z."""
     z = lm_head_logits(u, w_lm)
     lse = logsumexp_rows(z)
     zt = z[np.arange(z.shape[0]), np.asarray(ids, dtype=np.int64)]
+    if spread:
+        return lse - zt, lse, zt, z.std(axis=1)
     return lse - zt, lse, zt
 
 
@@ -178,15 +184,17 @@ def last_layer_hidden(q, k, v, w_o, cu_seqlens, diag="strict", scale=None,
 
 
 def last_layer_scores(q, k, v, w_o, w_lm, ids, cu_seqlens, diag="strict", scale=None,
-                      n_frozen=0, rows=None) -> np.ndarray:
-    """Surprise scores of the fast variant for the requested rows (all by default)."""
+                      n_frozen=0, rows=None, spread: bool = False):
+    """Surprise scores of the fast variant for the requested rows (all by default).
+    spread=True also returns the per-row logit spread (see surprise)."""
     cu = np.asarray(cu_seqlens, dtype=np.int64)
     N = int(cu[-1])
     rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
     u = last_layer_hidden(q, k, v, w_o, cu, diag, scale, rows)
-    s, _, _ = surprise(u, w_lm, np.asarray(ids)[rows])
+    out = surprise(u, w_lm, np.asarray(ids)[rows], spread=spread)
+    s = out[0]
     s[edge_rows(cu, n_frozen)[rows]] = np.inf
-    return s
+    return (s, out[3]) if spread else s
 
 
 def fused_lmhead_weight(w_lm, w_o) -> np.ndarray:
@@ -196,16 +204,17 @@ def fused_lmhead_weight(w_lm, w_o) -> np.ndarray:
 
 
 def last_layer_fused_scores(q, k, v, w_fused, ids, cu_seqlens, diag="strict", scale=None,
-                            n_frozen=0, rows=None) -> np.ndarray:
+                            n_frozen=0, rows=None, spread: bool = False):
     """Surprise scores of the fast variant with the LM head applied to the attention rows
     through a given product weight w_fused = W_lm W_o [V][Hq*d]."""
     cu = np.asarray(cu_seqlens, dtype=np.int64)
     N = int(cu[-1])
     rows = np.arange(N) if rows is None else np.asarray(rows, dtype=np.int64)
     y = attention_rows(q, k, v, cu, diag, scale, rows)
-    s, _, _ = surprise(y, w_fused, np.asarray(ids)[rows])
+    out = surprise(y, w_fused, np.asarray(ids)[rows], spread=spread)
+    s = out[0]
     s[edge_rows(cu, n_frozen)[rows]] = np.inf
-    return s
+    return (s, out[3]) if spread else s
 
 
 # ----------------------------------------------------------------------------------

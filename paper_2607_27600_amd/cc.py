@@ -98,7 +98,7 @@ def _load():
                                      _c_void_p]),
         "cc_pack_lmhead_bytes": (st, [_i64, _i32, sz]),
         "cc_pack_lmhead": (st, [_c_void_p, _i64, _i32, _c_void_p, ctypes.c_size_t, _c_void_p]),
-        "cc_lmhead_score_packed": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+        "cc_lmhead_score_packed": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p,
                                         _c_void_p, _c_void_p, _c_void_p, ctypes.c_size_t,
                                         _c_void_p]),
         "cc_fuse_wo_lmhead": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32,
@@ -241,7 +241,8 @@ class Inputs:
     keep: list = field(default_factory=list)
 
 
-def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[torch.Tensor] = None,
+def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: Optional[torch.Tensor] = None,
+           q: Optional[torch.Tensor] = None,
            w_o: Optional[torch.Tensor] = None, pos_ids: Optional[torch.Tensor] = None,
            embed: Optional[torch.Tensor] = None, layers: Optional[list] = None,
            final_norm: Optional[torch.Tensor] = None,
@@ -253,7 +254,7 @@ def inputs(*, kv: KV, token_ids: torch.Tensor, w_lm: torch.Tensor, q: Optional[t
     s.token_ids = token_ids.data_ptr()
     s.pos_ids = pos_ids.data_ptr() if pos_ids is not None else None
     s.w_o = w_o.data_ptr() if w_o is not None else None
-    s.w_lm = w_lm.data_ptr()
+    s.w_lm = w_lm.data_ptr() if w_lm is not None else None
     s.embed = embed.data_ptr() if embed is not None else None
     s.h_last = h_last.data_ptr() if h_last is not None else None
     s.w_lm_packed = w_lm_packed.data_ptr() if w_lm_packed is not None else None
@@ -335,12 +336,12 @@ def cc_pack_lmhead(x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=N
     return out
 
 
-def cc_lmhead_score_packed(p: Problem, u: torch.Tensor, w_lm: torch.Tensor, w_packed: torch.Tensor,
+def cc_lmhead_score_packed(p: Problem, u: torch.Tensor, w_packed: torch.Tensor,
                            token_ids: torch.Tensor, scores: torch.Tensor,
                            lse: Optional[torch.Tensor] = None, workspace=None, stream=None):
     if workspace is None:
         workspace = _workspace(cc_lmhead_workspace(p), p.device)
-    _check(_lib.cc_lmhead_score_packed(ctypes.byref(p.struct), _ptr(u), _ptr(w_lm), _ptr(w_packed),
+    _check(_lib.cc_lmhead_score_packed(ctypes.byref(p.struct), _ptr(u), _ptr(w_packed),
                                        _ptr(token_ids), _ptr(scores), _ptr(lse), _ptr(workspace),
                                        workspace.numel(), _stream(stream)),
            "cc_lmhead_score_packed")

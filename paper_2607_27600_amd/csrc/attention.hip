@@ -2,9 +2,9 @@
 // attends only to later entries j > i of its own sequence, reusing the stored keys and
 // values.  Output o[i][h] = sum_j softmax_j(scale * q[i][h] . k[j][c]) v[j][c], c = h/g.
 //
-// bf16 path (head_dim 128): flash-style, one workgroup of 4 waves per (sequence, KV head,
-// block of 128 "rows"), where a row is one (position, query head of the GQA group) pair,
-// so the g query heads that share a KV head share every K/V tile staged in LDS.
+// bf16 path (head_dim 128 or 64): flash-style, one workgroup of 4 waves per (sequence, KV
+// head, block of 128 "rows"), where a row is one (position, query head of the GQA group)
+// pair, so the g query heads that share a KV head share every K/V tile staged in LDS.
 //   S^T = K Q^T and O^T = V^T P^T on 32x32x16 bf16 MFMA.  Computing the transposed
 //   products leaves each lane owning one query row (column of the MFMA output), so the
 //   online-softmax statistics and rescaling stay in registers of that lane; the P tile
@@ -24,12 +24,36 @@ namespace cc {
 namespace {
 
 constexpr int BN = 64;            // keys per tile
-constexpr int HD = 128;           // head dim of the MFMA path
 constexpr int ROWS_W = 32;        // rows per wave
 constexpr int NWAVES = 4;
 constexpr int ROWS = ROWS_W * NWAVES;
-constexpr int TILE = BN * HD;     // elements of one K or V tile in LDS (16 KB, unpadded)
 constexpr float kRescale = 8.f;   // log2 headroom before the softmax reference max moves
+
+// Shape constants of the bf16 kernel for head dim HD (128 or 64).  A K or V tile is
+// BN x HD bf16 in LDS, unpadded, rows of 2 HD bytes in 16-byte chunks whose positions are
+// XOR-swizzled by bits of the row (key) index so that the fragment reads hit every bank
+// once per 16 lanes:
+//   HD = 128 (rows of 256 B = all 64 banks): K chunk c of row r at c ^ (r & 15); V chunk c
+//     at c ^ ((r & 3) << 2) (the transpose reads take 4 rows at a time);
+//   HD = 64 (rows of 128 B = half the banks, so rows r and r + 1 share no bank): K chunk c
+//     at c ^ ((r >> 1) & 7); V chunk c at c ^ (((r >> 1) & 1) << 2).
+template <int HD>
+struct Shape {
+  static_assert(HD == 128 || HD == 64, "head dim 128 or 64");
+  static constexpr int TILE = BN * HD;      // elements of one K or V tile (16 or 8 KB)
+  static constexpr int ROWB = HD * 2;       // bytes per tile row
+  static constexpr int CPR = HD / 8;        // 16-byte chunks per row
+  static constexpr int RPW = 64 / CPR;      // rows one wave-wide 1 KB load fills
+  static constexpr int NI = BN / (NWAVES * RPW);   // load instructions per wave per tile
+  static constexpr int NKS = HD / 16;       // k-steps of S^T = K Q^T
+  static constexpr int NDB = HD / 32;       // 32-dim blocks of O^T
+  static constexpr int NS = 2 * NKS;        // MFMAs of S^T per tile (two 32-key blocks)
+  static constexpr int NPV = 4 * NDB;       // MFMAs of O^T per tile (four 16-key steps)
+  __device__ static constexpr int kswz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
+  __device__ static constexpr int vswz(int r) {
+    return HD == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
+  }
+};
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void global_void;
@@ -74,8 +98,11 @@ struct SlabPages {
   int p[4];
 };
 
-template <bool PAGED>
+template <int HD, bool PAGED>
 __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
+  using SH = Shape<HD>;
+  constexpr int TILE = SH::TILE, ROWB = SH::ROWB, CPR = SH::CPR, RPW = SH::RPW, NI = SH::NI;
+  constexpr int NKS = SH::NKS, NDB = SH::NDB, NS = SH::NS, NPV = SH::NPV;
   // Two K and two V buffers as distinct objects: the compiler can then tell the buffer a
   // DMA is filling from the one being read, and waits for the DMA only where asked.
   __shared__ __attribute__((aligned(1024))) u16 kl0[TILE];
@@ -101,13 +128,13 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const int pos = valid ? row / g : n;
   const int hq = kvh * g + (valid ? row % g : 0);
 
-  // This lane's query row as the B operand of S^T = K Q^T: 8 k-steps of 16 dims,
+  // This lane's query row as the B operand of S^T = K Q^T: NKS k-steps of 16 dims,
   // lane half `hi` holds dims ks*16 + hi*8 .. +7.
-  bf16x8 qf[8];
+  bf16x8 qf[NKS];
   {
     const u16* qp = a.q + (int64_t(seq0 + (valid ? pos : 0)) * a.hq + hq) * HD + hi * 8;
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
       uint4 v = valid ? ld16(qp + ks * 16) : make_uint4(0, 0, 0, 0);
       qf[ks] = as_bf16x8(v);
     }
@@ -125,7 +152,7 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     if (valid) {
       u16* op = a.o + (int64_t(seq0 + pos) * a.hq + hq) * HD + hi * 4;
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
           *reinterpret_cast<uint2*>(op + db * 32 + jj * 8) = make_uint2(0, 0);
@@ -136,15 +163,17 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const int tm0 = min(te, max(tb, (pos_hi_wg + 1 + BN - 1) / BN));
   const int tm1 = (n % BN == 0) ? te : te - 1;
 
-  // ---- tile DMA (global -> LDS, no registers).  Wave w, instruction i fills tile rows
-  // 16i + 4w .. +3 (1 KB): lane l writes row 16i + 4w + l/16 at 16-byte position l%16, and
-  // loads the row's chunk (l%16) ^ swz(row) there, swz = row & 15 for K and
-  // (row & 3) << 2 for V.  Rows past the sequence end are clamped to its last key (their
-  // weights are 0 and the clamped data is finite).
+  // ---- tile DMA (global -> LDS, no registers).  Wave w, instruction i fills the RPW tile
+  // rows starting at R = 4 RPW i + RPW w (1 KB): lane l writes row R + l / CPR at 16-byte
+  // position l % CPR, and loads the row's chunk (l % CPR) ^ swz(row) there (the swizzles of
+  // Shape).  The rows of one instruction lie in one 16-key slab (keys 16 s .. 16 s + 15,
+  // s = R / 16); drow = R % 16 + l / CPR is the lane's row within the slab.  Rows past the
+  // sequence end are clamped to its last key (their weights are 0 and the clamped data is
+  // finite).
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int drow = 4 * wave + (lane >> 4);
-  const int kch = (lane & 15) ^ (drow & 15);
-  const int vch = (lane & 15) ^ ((drow & 3) << 2);
+  const int drow = (RPW * NWAVES > 16 ? (wave * RPW) % 16 : wave * RPW) + lane / CPR;
+  const int kch = (lane % CPR) ^ SH::kswz(drow);
+  const int vch = (lane % CPR) ^ SH::vswz(drow);
   const char* kbase = reinterpret_cast<const char*>(a.k.base);
   const char* vbase = reinterpret_cast<const char*>(a.v.base);
   const int64_t kts = a.k.tok_stride * 2, vts = a.v.tok_stride * 2;   // bytes per key
@@ -164,62 +193,84 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
       s.p[i] = PAGED ? btab[min((t * BN + 16 * i) >> a.k.page_shift, last_page)] : 0;
     return s;
   };
+  // The 16-key slab of load instruction i (wave-uniform): at HD = 128 the four waves' rows
+  // of one instruction form slab i; at HD = 64 waves 0-1 fill slab 2i and waves 2-3 slab
+  // 2i + 1.  The page of that slab is picked without indexing the array by a variable.
+  auto slab_of = [&](int i) {
+    return RPW * NWAVES > 16 ? (RPW * NWAVES / 16) * i + (RPW * wave_u) / 16 : i;
+  };
+  auto slab_page = [&](const SlabPages& pg, int i) {
+    if constexpr (RPW * NWAVES > 16)
+      return (wave_u >> 1) ? pg.p[2 * i + 1] : pg.p[2 * i];
+    else
+      return pg.p[i];
+  };
   // Fill an LDS tile with tile t.  Full tiles: a uniform base per slab plus the lane's fixed
   // offset.  The last, partial tile: per-lane rows (clamped), per-lane page lookups.
   auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, uint32_t lane_off,
                    int ch, int64_t ts, const SlabPages& pg) {
     const int key0 = t * BN;
-    u16* lds = dst + wave_u * 4 * HD;
+    u16* lds = dst + wave_u * RPW * HD;
     if (key0 + BN <= n) {
       // keep the 32-bit offset opaque here so that it is not widened outside the loop
       asm volatile("" : "+v"(lane_off));
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < NI; ++i) {
+        const int si = slab_of(i);
         int64_t slab;
         if constexpr (PAGED)
-          slab = int64_t(pg.p[i]) * kv.page_stride + int64_t((key0 + 16 * i) & kv.page_mask) * kv.tok_stride;
+          slab = int64_t(slab_page(pg, i)) * kv.page_stride + int64_t((key0 + 16 * si) & kv.page_mask) * kv.tok_stride;
         else
-          slab = int64_t(key0 + 16 * i) * kv.tok_stride;
+          slab = int64_t(key0 + 16 * si) * kv.tok_stride;
         const char* base = uniform_ptr(plane + slab * 2);
         __builtin_amdgcn_global_load_lds((global_void*)(base + lane_off),
-                                         (lds_void*)(lds + i * 16 * HD), 16, 0, 0);
+                                         (lds_void*)(lds + i * NWAVES * RPW * HD), 16, 0, 0);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = min(key0 + 16 * i + drow, n - 1);
+      for (int i = 0; i < NI; ++i) {
+        const int key = min(key0 + 16 * slab_of(i) + drow, n - 1);
         int64_t off;
         if constexpr (PAGED)
           off = int64_t(btab[key >> kv.page_shift]) * kv.page_stride + int64_t(key & kv.page_mask) * kv.tok_stride;
         else
           off = int64_t(key) * kv.tok_stride;
         __builtin_amdgcn_global_load_lds((global_void*)(plane + off * 2 + ch * 16),
-                                         (lds_void*)(lds + i * 16 * HD), 16, 0, 0);
+                                         (lds_void*)(lds + i * NWAVES * RPW * HD), 16, 0, 0);
       }
     }
   };
 
   // ---- fragment reads.  K (A operand of S^T = K Q^T): MFMA j reads row (j&1)*32 + col,
   // chunk 2*(j>>1) + hi.  V^T (A operand of O^T = V^T P^T): MFMA j = (k-step kk, d block db)
-  // needs d = 32 db + col and keys 16kk + 4hi + {0..3}, 16kk + 8 + 4hi + {0..3} (the order
-  // of the P operand's k-slots): two transpose reads of 4 keys x 16 dims.
-  uint32_t koff[8];
+  // = (j / NDB, j % NDB) needs d = 32 db + col and keys 16kk + 4hi + {0..3},
+  // 16kk + 8 + 4hi + {0..3} (the order of the P operand's k-slots): two transpose reads of
+  // 4 keys x 16 dims.  Lane 4y + c of lane group G reads key row 4 (G >> 1) + y at dims
+  // 32 db + 16 (G & 1) + 4 c .. +3, i.e. 8-byte half (c & 1) of chunk
+  // 4 db + 2 (G & 1) + (c >> 1), at that chunk's swizzled position.
+  uint32_t koff[NKS];
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj) koff[jj] = col * 256 + 16 * ((2 * jj + hi) ^ (col & 15));
-  uint32_t voff[4];
+  for (int jj = 0; jj < NKS; ++jj) koff[jj] = col * ROWB + 16 * ((2 * jj + hi) ^ SH::kswz(col));
+  uint32_t voff[NDB];
   {
     const int G = lane >> 4, L = lane & 15, y = L >> 2;
+    const int r = 4 * (G >> 1) + y;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-      voff[db] = (4 * (G >> 1) + y) * 256 + 64 * (db ^ y) + 32 * (G & 1) + 8 * (L & 3);
+    for (int db = 0; db < NDB; ++db) {
+      if constexpr (HD == 128)   // vswz(r) = 4 y: the swizzle moves whole 64-byte groups
+        voff[db] = r * ROWB + 64 * (db ^ y) + 32 * (G & 1) + 8 * (L & 3);
+      else
+        voff[db] = r * ROWB + 16 * ((4 * db + 2 * (G & 1) + ((L & 3) >> 1)) ^ SH::vswz(r)) +
+                   8 * (L & 1);
+    }
   }
   auto kfrag = [&](const u16* Kl, int j) {
     return as_bf16x8(*reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(Kl) +
-                                                     koff[j >> 1] + (j & 1) * 8192));
+                                                     koff[j >> 1] + (j & 1) * (32 * ROWB)));
   };
   auto vfrag = [&](const u16* Vl, int j) {
-    const char* p = reinterpret_cast<const char*>(Vl) + voff[j & 3] + (j >> 2) * 4096;
-    const v4i16 lo = ds_read_tr(p), hi2 = ds_read_tr(p + 2048);
+    const char* p = reinterpret_cast<const char*>(Vl) + voff[j % NDB] + (j / NDB) * (16 * ROWB);
+    const v4i16 lo = ds_read_tr(p), hi2 = ds_read_tr(p + 8 * ROWB);
     const v8i16 both = __builtin_shufflevector(lo, hi2, 0, 1, 2, 3, 4, 5, 6, 7);
     return __builtin_bit_cast(bf16x8, both);
   };
@@ -250,9 +301,9 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   };
 
   float m_run = -INFINITY, l_run = 0.f;
-  f32x16 acc[4];
+  f32x16 acc[NDB];
 #pragma unroll
-  for (int db = 0; db < 4; ++db) acc[db] = f32x16{};
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
 
   // prologue: K(tb), V(tb), K(tb+1) in LDS; S(tb) and its unmasked row max in registers.
   // Page numbers: pk for the K tile of the next step (t+2), pv for its V tile (t+1), pn
@@ -272,13 +323,13 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   sa[0] = f32x16{};
   sa[1] = f32x16{};
 #pragma unroll
-  for (int j = 0; j < 16; ++j) sa[j & 1] = mfma32(kfrag(kl0, j), qf[j >> 1], sa[j & 1]);
+  for (int j = 0; j < NS; ++j) sa[j & 1] = mfma32(kfrag(kl0, j), qf[j >> 1], sa[j & 1]);
   float mx = row_max(sa);
 
   // Tile t with parity P = (t - tb) & 1.  S(t) is in sc with its unmasked row max in mx;
   // K(t+1) in kl[1-P], V(t) in vl[P].  The DMAs of K(t+2) -> kl[P] and V(t+1) -> vl[1-P]
-  // refill buffers freed by the previous tile.  Issue order: the 16 MFMAs of S(t+1) carry
-  // the exponentials of tile t; the 16 MFMAs of P V carry the bf16 packing of P, the row
+  // refill buffers freed by the previous tile.  Issue order: the NS MFMAs of S(t+1) carry
+  // the 32 exponentials of tile t; the NPV MFMAs of P V carry the bf16 packing of P, the row
   // sums and the row max of S(t+1).  sched_barrier fences keep the compiler from regrouping.
   auto step = [&](int t, auto par, bool masked) {
     constexpr int P = decltype(par)::value;
@@ -318,13 +369,14 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     // (measured: 4-7% faster at n = 4096, 1.5% at 32768; the same priority over both
     // sections, or over the P V section, gains less or nothing).
     __builtin_amdgcn_s_setprio(1);
+    constexpr int EPM = 32 / NS;   // exponentials per MFMA
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j + 3 < 16) kf[(j + 3) & 3] = kfrag(Kn, j + 3);
+    for (int j = 0; j < NS; ++j) {
+      if (j + 3 < NS) kf[(j + 3) & 3] = kfrag(Kn, j + 3);
       sn[j & 1] = mfma32(kf[j & 3], qf[j >> 1], sn[j & 1]);
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int f = 2 * j + u, mb = f >> 4, e = f & 15;
+      for (int u = 0; u < EPM; ++u) {
+        const int f = EPM * j + u, mb = f >> 4, e = f & 15;
         const float p = fast_exp2(fmaf(sc[mb][e], a.c2, -mc));
         // pin the exponential here, between the MFMAs, instead of next to its later uses
         asm volatile("" ::"v"(p));
@@ -334,7 +386,7 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     }
     if (__any(corr != 1.f)) {
 #pragma unroll
-      for (int db = 0; db < 4; ++db) acc[db] *= corr;
+      for (int db = 0; db < NDB; ++db) acc[db] *= corr;
     }
     // P^T operand: k-step kk covers keys 16kk .. 16kk+15; lane half hi holds keys
     // {4hi..4hi+3, 8+4hi..8+4hi+3} of that step, i.e. S^T entries 8*(kk%2)..+7 of block kk/2
@@ -350,16 +402,31 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     __builtin_amdgcn_s_setprio(0);
     pack(0);
     float ls0 = 0.f, ls1 = 0.f, m0 = -INFINITY, m1 = -INFINITY;
+    constexpr int SPM = 32 / NPV;   // row-sum terms per MFMA
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j + 3 < 16) vf[(j + 3) & 3] = vfrag(Vc, j + 3);
-      acc[j & 3] = mfma32(vf[j & 3], pf[j >> 2], acc[j & 3]);
-      if ((j & 3) == 3 && j < 15) pack((j >> 2) + 1);
-      ls0 += sc[j >> 3][(2 * j) & 15];
-      ls1 += sc[j >> 3][(2 * j + 1) & 15];
+    for (int j = 0; j < NPV; ++j) {
+      if (j + 3 < NPV) vf[(j + 3) & 3] = vfrag(Vc, j + 3);
+      acc[j % NDB] = mfma32(vf[j & 3], pf[j / NDB], acc[j % NDB]);
+      if (j % NDB == NDB - 1 && j < NPV - 1) pack(j / NDB + 1);
+#pragma unroll
+      for (int u = 0; u < SPM; u += 2) {
+        ls0 += sc[(SPM * j + u) >> 4][(SPM * j + u) & 15];
+        ls1 += sc[(SPM * j + u + 1) >> 4][(SPM * j + u + 1) & 15];
+      }
       asm volatile("" : "+v"(ls0), "+v"(ls1));
-      if (j >= 2) {
+      if constexpr (HD == 64) {
+        // row max of S(t+1) over slots 2..7: six entries per slot (sn[0] then sn[1])
+        if (j >= 2) {
+#pragma unroll
+          for (int u = 0; u < 6; ++u) {
+            const int f = 6 * (j - 2) + u;
+            if (f < 16) m0 = fmaxf(m0, sn[0][f]);
+            else if (f < 32) m1 = fmaxf(m1, sn[1][f - 16]);
+          }
+          asm volatile("" : "+v"(m0), "+v"(m1));
+        }
+      } else if (j >= 2) {
         // row max of S(t+1), whose MFMAs were issued during the exponentials: 32 entries
         // over slots 2..12
         const int f = j - 2;
@@ -393,27 +460,28 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   // The output goes out through LDS as whole rows.  The K buffers are free here (the last
-  // step waited for every load and ended with a barrier); each wave stages its 32 rows x 128
-  // dims (8 KB, 16-byte chunk c of row r at chunk c ^ (r & 15), so both the 8-byte writes of
-  // the lane halves and the 16-byte row reads hit every bank once), then writes 16 bytes per
-  // lane along the rows.  The g rows of one position are adjacent in o (head-major), so a
-  // wave instruction stores 1 KB of whole rows instead of 64 scattered 8-byte pieces.  LDS
-  // operations of one wave complete in order, so the wave needs no barrier of its own.
-  char* stg = reinterpret_cast<char*>(wave < 2 ? kl0 : kl1) + (wave & 1) * (ROWS_W * HD * 2);
+  // step waited for every load and ended with a barrier); each wave stages its 32 rows x HD
+  // dims (16-byte chunk c of row r at chunk c ^ kswz(r), so the 16-byte row reads hit every
+  // bank once, and at HD = 128 the 8-byte writes of the lane halves too), then writes 16
+  // bytes per lane along the rows.  The g rows of one position are adjacent in o
+  // (head-major), so a wave instruction stores 1 KB of whole rows instead of 64 scattered
+  // 8-byte pieces.  LDS operations of one wave complete in order, so the wave needs no
+  // barrier of its own.
+  char* stg = reinterpret_cast<char*>(wave < 2 ? kl0 : kl1) + (wave & 1) * (ROWS_W * ROWB);
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
       bf16x4 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = (__bf16)(acc[db][jj * 4 + e] * inv);
       const int c = db * 4 + jj;
-      *reinterpret_cast<bf16x4*>(stg + col * (HD * 2) + ((c ^ (col & 15)) * 16) + hi * 8) = o;
+      *reinterpret_cast<bf16x4*>(stg + col * ROWB + ((c ^ SH::kswz(col)) * 16) + hi * 8) = o;
     }
 #pragma unroll
-  for (int i = 0; i < ROWS_W / 4; ++i) {
-    const int r = 4 * i + (lane >> 4), c = lane & 15;
-    const uint4 v = *reinterpret_cast<const uint4*>(stg + r * (HD * 2) + ((c ^ (r & 15)) * 16));
+  for (int i = 0; i < ROWS_W * CPR / 64; ++i) {
+    const int r = RPW * i + lane / CPR, c = lane % CPR;
+    const uint4 v = *reinterpret_cast<const uint4*>(stg + r * ROWB + ((c ^ SH::kswz(r)) * 16));
     const int orow = rb * ROWS + wave * ROWS_W + r;
     if (orow < nrows) {
       const int opos = orow / g, ohq = kvh * g + orow % g;
@@ -539,10 +607,17 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
     x.q = static_cast<const u16*>(a.q);
     x.o = static_cast<u16*>(a.o);
     x.c2 = a.scale * kLog2e;
-    if (a.paged)
-      hipLaunchKernelGGL(attn_cc_bf16<true>, dim3(a.n_work), dim3(256), 0, s, x);
-    else
-      hipLaunchKernelGGL(attn_cc_bf16<false>, dim3(a.n_work), dim3(256), 0, s, x);
+    if (a.head_dim == 64) {
+      if (a.paged)
+        hipLaunchKernelGGL((attn_cc_bf16<64, true>), dim3(a.n_work), dim3(256), 0, s, x);
+      else
+        hipLaunchKernelGGL((attn_cc_bf16<64, false>), dim3(a.n_work), dim3(256), 0, s, x);
+    } else {
+      if (a.paged)
+        hipLaunchKernelGGL((attn_cc_bf16<128, true>), dim3(a.n_work), dim3(256), 0, s, x);
+      else
+        hipLaunchKernelGGL((attn_cc_bf16<128, false>), dim3(a.n_work), dim3(256), 0, s, x);
+    }
     return hipGetLastError();
   }
   AttnArgsF x;

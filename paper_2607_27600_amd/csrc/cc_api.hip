@@ -46,15 +46,14 @@ cc_status check_problem(const cc_problem* p) {
   if (p->head_dim < 1 || p->hidden < 1 || p->vocab < 1) return CC_ERR_SHAPE;
   if (p->n_frozen < 0) return CC_ERR_ARG;
   if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.f) return CC_ERR_ARG;
-  if (p->dtype == CC_BF16) {
-    if (p->head_dim != 128) return CC_ERR_UNSUPPORTED;
-    if (p->hidden % 64 != 0) return CC_ERR_UNSUPPORTED;
-  } else {
-    if (p->head_dim != 64 && p->head_dim != 128) return CC_ERR_UNSUPPORTED;
-  }
+  if (p->head_dim != 64 && p->head_dim != 128) return CC_ERR_UNSUPPORTED;
+  // bf16 projections and the LM head step K in 64-element tiles
+  if (p->dtype == CC_BF16 && p->hidden % 64 != 0) return CC_ERR_UNSUPPORTED;
   if (p->mode == CC_MODE_FULL || p->mode == CC_MODE_LAST_LAYER_H) {
     if ((p->mode == CC_MODE_FULL && p->n_layers < 1) || p->ffn < 1) return CC_ERR_SHAPE;
     if (p->dtype != CC_BF16) return CC_ERR_UNSUPPORTED;
+    // the W_q epilogue applies RoPE with one wave's 128 rows spanning exactly one head
+    if (p->head_dim != 128) return CC_ERR_UNSUPPORTED;
     if (p->ffn % 64 != 0) return CC_ERR_UNSUPPORTED;
     if (!(p->rope_theta > 0.f) || !(p->rms_eps >= 0.f)) return CC_ERR_ARG;
   }
@@ -293,6 +292,11 @@ cc_status run_lmhead(const cc_problem* p, const void* u, const void* w_lm, const
   return CC_OK;
 }
 
+// The row-major LM head weight, needed unless the packed one is used.
+bool lm_weight_ok(const cc_problem* p, const void* w_lm) {
+  return p->lmhead_packed || (w_lm && aligned16(w_lm));
+}
+
 // The packed LM head needs its weight (checked before anything is launched).
 cc_status check_packed(const cc_problem* p, const void* w_packed) {
   if (!p->lmhead_packed || n_tokens(p) == 0) return CC_OK;
@@ -314,11 +318,10 @@ cc_status score_full(const cc_problem* p, const cc_inputs* in, float* scores, vo
                      size_t ws_bytes, void* stream) {
   CC_TRY(check_kv(p, &in->kv, p->n_layers));
   const int N = n_tokens(p);
-  if (N > 0 && (!in->embed || !in->layers_h || !in->final_norm || !in->w_lm || !in->token_ids ||
-                !scores))
+  if (N > 0 && (!in->embed || !in->layers_h || !in->final_norm || !in->token_ids || !scores))
     return CC_ERR_ARG;
   if (N > 0) {
-    if (!aligned16(in->embed) || !aligned16(in->w_lm) || !aligned16(in->final_norm))
+    if (!aligned16(in->embed) || !lm_weight_ok(p, in->w_lm) || !aligned16(in->final_norm))
       return CC_ERR_ARG;
     for (int l = 0; l < p->n_layers; ++l) {
       const cc_layer_weights& W = in->layers_h[l];
@@ -365,11 +368,10 @@ cc_status score_last_h(const cc_problem* p, const cc_inputs* in, float* scores, 
                        size_t ws_bytes, void* stream) {
   CC_TRY(check_kv(p, &in->kv, 1));
   const int N = n_tokens(p);
-  if (N > 0 && (!in->h_last || !in->layers_h || !in->final_norm || !in->w_lm ||
-                !in->token_ids || !scores))
+  if (N > 0 && (!in->h_last || !in->layers_h || !in->final_norm || !in->token_ids || !scores))
     return CC_ERR_ARG;
   if (N > 0) {
-    if (!aligned16(in->h_last) || !aligned16(in->w_lm) || !aligned16(in->final_norm))
+    if (!aligned16(in->h_last) || !lm_weight_ok(p, in->w_lm) || !aligned16(in->final_norm))
       return CC_ERR_ARG;
     const cc_layer_weights& W = in->layers_h[0];
     const void* ptrs[7] = {W.attn_norm, W.wq, W.wo, W.mlp_norm, W.w_gate, W.w_up, W.w_down};
@@ -460,18 +462,17 @@ cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
   return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream));
 }
 
-cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_lm,
-                                 const void* w_packed, const int32_t* token_ids,
-                                 float* scores, float* lse, void* ws, size_t ws_bytes,
-                                 void* stream) {
+cc_status cc_lmhead_score_packed(const cc_problem* p, const void* u, const void* w_packed,
+                                 const int32_t* token_ids, float* scores, float* lse, void* ws,
+                                 size_t ws_bytes, void* stream) {
   CC_TRY(check_problem(p));
   if (!p->lmhead_packed) return CC_ERR_ARG;
-  if (n_tokens(p) > 0 && (!u || !w_lm || !token_ids || !scores)) return CC_ERR_ARG;
-  if (!aligned16(u) || !aligned16(w_lm)) return CC_ERR_ARG;
+  if (n_tokens(p) > 0 && (!u || !token_ids || !scores)) return CC_ERR_ARG;
+  if (!aligned16(u)) return CC_ERR_ARG;
   CC_TRY(check_packed(p, w_packed));
   CC_TRY(check_ws(ws, ws_bytes, lmhead_ws_bytes(p)));
-  return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream), 0,
-                    w_packed);
+  return run_lmhead(p, u, nullptr, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream),
+                    0, w_packed);
 }
 
 cc_status cc_pack_lmhead_bytes(int64_t rows, int32_t cols, size_t* bytes) {
@@ -524,10 +525,10 @@ cc_status cc_score(const cc_problem* p, const cc_inputs* in, float* scores, void
   CC_TRY(check_kv(p, &in->kv, 1));
   const int N = n_tokens(p);
   const bool fused = p->mode == CC_MODE_LAST_LAYER_FUSED;
-  if (N > 0 && (!in->q || (!fused && !in->w_o) || !in->w_lm || !in->token_ids || !scores))
-    return CC_ERR_ARG;
+  if (N > 0 && (!in->q || (!fused && !in->w_o) || !in->token_ids || !scores)) return CC_ERR_ARG;
+  if (N > 0 && !p->lmhead_packed && !in->w_lm) return CC_ERR_ARG;
   if (p->dtype == CC_BF16 &&
-      (!aligned16(in->q) || (!fused && !aligned16(in->w_o)) || !aligned16(in->w_lm)))
+      (!aligned16(in->q) || (!fused && !aligned16(in->w_o)) || !lm_weight_ok(p, in->w_lm)))
     return CC_ERR_ARG;
   CC_TRY(check_packed(p, in->w_lm_packed));
   const ScoreLayout L = score_layout(p);

@@ -2,10 +2,10 @@
 //
 //   y = x W^T          the layer's output projection of the fast variant (Sec. 3.1)
 //   LM head + LSE      z = W_lm u for every cached entry, reduced on the fly to a
-//                      per-(entry, vocabulary tile) pair (max z, sum exp(z - max)) and
-//                      the target logit z[x_i]; a combine kernel turns these into
-//                      logsumexp(z) - z[x_i] (Eq. (5) read as -log P).  The [N][V] logits
-//                      never leave registers.
+//                      per-(entry, vocabulary tile) pair (max z, sum exp(z - max)); the
+//                      lane that holds z[x_i] in its accumulators writes the target logit
+//                      from them; a combine kernel turns these into logsumexp(z) - z[x_i]
+//                      (Eq. (5) read as -log P).  The [N][V] logits never leave registers.
 //
 // bf16 kernel: C[m][n] = sum_k A[m][k] B[n][k] with both operands K-contiguous, a 256x256
 // workgroup tile, 8 waves (two per SIMD, so one wave's barrier and load waits hide behind
@@ -69,11 +69,18 @@ struct EpiStore {
 // the workgroup's 256 vocabulary rows.  The whole epilogue runs while the matrix cores
 // idle, so it is kept to one max and one exp-accumulate per logit; only workgroups on the
 // vocabulary edge take the masked variant.
+// Target gather: the cached token x_n of entry n lies in exactly one vocabulary tile, one
+// wave row of it and one lane half; that lane writes target[n] = its accumulator for row
+// x_n (times the scales below), so the target logit and the log-sum-exp come from the
+// same accumulators.  The ids are loaded first and the selection runs only in waves where
+// some lane owns a target (about 3% of them at a vocabulary of 128k).
 // An FP8 LM head passes the dequantization scales: the logit is acc * sw * su[n]
 // (su per entry, sw for the whole matrix); without them the factor is 1 and the
 // arithmetic is unchanged.
 struct EpiLse {
   float2* partial;
+  float* target;               // [N] target logits z[x_n]
+  const int32_t* ids;          // [N] cached token ids
   const float* su = nullptr;   // [N] per-entry scale, or null
   const float* sw = nullptr;   // [1] matrix scale (device), with su
   template <bool EDGE>
@@ -118,6 +125,11 @@ struct EpiLse {
     const int wave = threadIdx.x >> 6;
     const int wm = wave / WGN, wn = wave % WGN;
     float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
+    // target rows relative to this wave's first vocabulary row (loaded before the
+    // reduction so their latency hides behind it)
+    int rt[GNB];
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) rt[nb] = ids[min(n0w + nb * 32 + col, g.N - 1)] - m0w;
     float f[GNB];
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb)
@@ -127,6 +139,23 @@ struct EpiLse {
       reduce<false>(acc, g.M, m0w, hi, f, mx, sm);
     else
       reduce<true>(acc, g.M, m0w, hi, f, mx, sm);
+    // row r of the wave's 128 sits in block r / 32, element 4 ((r % 32) / 8) + r % 4 of the
+    // lane half (r / 4) % 2
+#pragma unroll
+    for (int nb = 0; nb < GNB; ++nb) {
+      const int r = rt[nb];
+      const bool own = n0w + nb * 32 + col < g.N && uint32_t(r) < uint32_t(GTM) &&
+                       ((r >> 2) & 1) == hi;
+      if (__any(own)) {
+        const int idx = (r >> 5) * 16 + ((r & 31) >> 3) * 4 + (r & 3);
+        float z = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < GMB; ++mb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) z = idx == mb * 16 + e ? acc[mb][nb][e] : z;
+        if (own) target[n0w + nb * 32 + col] = z * f[nb];
+      }
+    }
 #pragma unroll
     for (int nb = 0; nb < GNB; ++nb) {
       // combine the two lane halves (rows 4*hi..)
@@ -577,9 +606,13 @@ __global__ __launch_bounds__(256) void pack_rows_kernel(const u16* __restrict__ 
 }
 
 // LSE epilogue in the 16x16 layout: each lane holds 32 logits of each of four entries; the
-// four lane groups of an entry combine by shuffles, the two wave rows through LDS.
+// four lane groups of an entry combine by shuffles, the two wave rows through LDS.  The
+// target logit is gathered from the accumulators as in EpiLse: row r of the wave's 128 sits
+// in block r / 16, element r % 4 of lane group (r / 4) % 4.
 struct EpiLse16 {
   float2* partial;
+  float* target;         // [N] target logits z[x_n]
+  const int32_t* ids;    // [N] cached token ids
   __device__ void operator()(const f32x4 (&acc)[HMB][HNB], const GemmArgs& g, int tm, int m0w,
                              int n0w, int lane, u16* lds) const {
     const int grp = lane >> 4, c16 = lane & 15;
@@ -587,6 +620,9 @@ struct EpiLse16 {
     const int wm = wave / WGN, wn = wave % WGN;
     float2* red = reinterpret_cast<float2*>(lds);   // [WGM][GBN] pairs
     const bool edge = tm * GBM + GBM > g.M;
+    int rt[HNB];
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) rt[nb] = ids[min(n0w + nb * 16 + c16, g.N - 1)] - m0w;
     float mx[HNB], sm[HNB], mc[HNB];
 #pragma unroll
     for (int nb = 0; nb < HNB; ++nb) mx[nb] = -INFINITY;
@@ -613,6 +649,21 @@ struct EpiLse16 {
         for (int nb = 0; nb < HNB; ++nb)
           if (ok) sm[nb] += fast_exp2(fmaf(acc[mb][nb][e], kLog2e, -mc[nb]));
       }
+#pragma unroll
+    for (int nb = 0; nb < HNB; ++nb) {
+      const int r = rt[nb];
+      const bool own = n0w + nb * 16 + c16 < g.N && uint32_t(r) < uint32_t(GTM) &&
+                       ((r >> 2) & 3) == grp;
+      if (__any(own)) {
+        const int idx = (r >> 4) * 4 + (r & 3);
+        float z = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < HMB; ++mb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z = idx == mb * 4 + e ? acc[mb][nb][e] : z;
+        if (own) target[n0w + nb * 16 + c16] = z;
+      }
+    }
 #pragma unroll
     for (int nb = 0; nb < HNB; ++nb) {
 #pragma unroll
@@ -985,34 +1036,6 @@ __global__ __launch_bounds__(256) void quantize_matrix_kernel(const T* __restric
   quantize_row<T>(x + r * cols, cols, amax[0], q + r * cols);
 }
 
-// z[x_n] of the FP8 head: one wave per entry, the decoded codes' dot product times the
-// two scales
-__global__ __launch_bounds__(256) void target_logit_fp8(const uint8_t* __restrict__ uq,
-                                                        const uint8_t* __restrict__ wq,
-                                                        const float* __restrict__ su,
-                                                        const float* __restrict__ sw,
-                                                        const int32_t* __restrict__ ids,
-                                                        float* __restrict__ target, int N, int D) {
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (n >= N) return;
-  const uint32_t* ur = reinterpret_cast<const uint32_t*>(uq + int64_t(n) * D);
-  const uint32_t* wr = reinterpret_cast<const uint32_t*>(wq + int64_t(ids[n]) * D);
-  float acc = 0.f;
-  for (int i = lane; i < D / 4; i += 64) {
-    const int a = int(ur[i]), b = int(wr[i]);
-    const auto a0 = __builtin_amdgcn_cvt_pk_f32_fp8(a, false), a1 = __builtin_amdgcn_cvt_pk_f32_fp8(a, true);
-    const auto b0 = __builtin_amdgcn_cvt_pk_f32_fp8(b, false), b1 = __builtin_amdgcn_cvt_pk_f32_fp8(b, true);
-    acc = fmaf(a0[0], b0[0], acc);
-    acc = fmaf(a0[1], b0[1], acc);
-    acc = fmaf(a1[0], b1[0], acc);
-    acc = fmaf(a1[1], b1[1], acc);
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) target[n] = acc * su[n] * sw[0];
-}
-
 // ------------------------------------------------------------------ fp32 path
 
 constexpr int FT = 64, FK = 16;
@@ -1112,47 +1135,6 @@ __global__ __launch_bounds__(256) void gemm_tn_f32(GemmArgsF g, Epi epi) {
 
 // ------------------------------------------------------------------ LSE combine
 
-// The logit of the cached token, z_i[x_i] = W_lm[x_i] . u_i, one wave per entry with fp32
-// accumulation (the same products the LM-head GEMM accumulates, in another order).
-template <typename T>
-__device__ __forceinline__ float ldf(const T* p, int64_t i);
-template <>
-__device__ __forceinline__ float ldf<u16>(const u16* p, int64_t i) { return bf2f(p[i]); }
-template <>
-__device__ __forceinline__ float ldf<float>(const float* p, int64_t i) { return p[i]; }
-
-template <typename T>
-__global__ __launch_bounds__(256) void target_logit(const T* __restrict__ u,
-                                                    const T* __restrict__ w,
-                                                    const int32_t* __restrict__ ids,
-                                                    float* __restrict__ target, int N, int D) {
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (n >= N) return;
-  const T* ur = u + int64_t(n) * D;
-  const T* wr = w + int64_t(ids[n]) * D;
-  float acc = 0.f;
-  if constexpr (sizeof(T) == 2) {
-    // 16-byte loads: 8 bf16 per lane per step, all steps' loads independent
-    for (int i = lane * 8; i < D; i += 512) {
-      const uint4 a = *reinterpret_cast<const uint4*>(ur + i);
-      const uint4 b = *reinterpret_cast<const uint4*>(wr + i);
-      const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc = fmaf(__uint_as_float(av[q] << 16), __uint_as_float(bv[q] << 16), acc);
-        acc = fmaf(__uint_as_float(av[q] & 0xffff0000u), __uint_as_float(bv[q] & 0xffff0000u),
-                   acc);
-      }
-    }
-  } else {
-    for (int i = lane; i < D; i += 64) acc = fmaf(ldf<T>(ur, i), ldf<T>(wr, i), acc);
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) target[n] = acc;
-}
-
 // One workgroup per 16 entries: thread (group gi, entry e) folds the vocabulary tiles
 // gi, gi+64, ... of entry e (16 consecutive entries read 128 contiguous bytes of a tile's
 // row of partials; up to 512 tiles are eight loads per thread, all in flight at once), then
@@ -1214,7 +1196,11 @@ __global__ __launch_bounds__(CMB_E * CMB_G) void lse_combine(const float2* parti
     }
     const bool last = n == cu[lo + 1] - 1;
     const bool frozen = n - cu[lo] < n_frozen;
-    scores[n] = (last || frozen) ? INFINITY : lse - target[n];
+    // -log P >= 0: for a near-certain token (z[x_n] the row maximum, every other term
+    // tiny) rounding in the exponentials and the logarithm can take the difference a few
+    // ulps below zero; it is clamped there (a NaN stays NaN)
+    const float d = lse - target[n];
+    scores[n] = (last || frozen) ? INFINITY : (d < 0.f ? 0.f : d);
     if (lse_out) lse_out[n] = lse;
   }
 }
@@ -1323,12 +1309,8 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
     g.tiles_n = (a.N + GBN - 1) / GBN;
     n_vt = (a.V + GBM - 1) / GBM;
     g.tiles_m = n_vt;
-    EpiLse16 e{a.partial};
+    EpiLse16 e{a.partial, a.target, a.ids};
     hipLaunchKernelGGL(gemm_lmhead_packed<EpiLse16>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
-    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
-    hipLaunchKernelGGL(target_logit<u16>, dim3((a.N + 3) / 4), dim3(256), 0, s,
-                       static_cast<const u16*>(a.u), static_cast<const u16*>(a.w_lm), a.ids,
-                       a.target, a.N, a.D);
   } else if (a.dtype == CC_BF16) {
     GemmArgs g;
     g.A2 = nullptr;
@@ -1342,12 +1324,8 @@ hipError_t launch_lmhead(const LmHeadLaunch& a, hipStream_t s) {
     g.tiles_n = (a.N + GBN - 1) / GBN;
     n_vt = (a.V + GBM - 1) / GBM;
     g.tiles_m = n_vt;
-    EpiLse e{a.partial};
+    EpiLse e{a.partial, a.target, a.ids};
     hipLaunchKernelGGL(gemm_tn_bf16<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
-    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
-    hipLaunchKernelGGL(target_logit<u16>, dim3((a.N + 3) / 4), dim3(256), 0, s,
-                       static_cast<const u16*>(a.u), static_cast<const u16*>(a.w_lm), a.ids,
-                       a.target, a.N, a.D);
   } else {
     GemmArgsF g;
     g.A = static_cast<const float*>(a.w_lm);
@@ -1415,11 +1393,8 @@ hipError_t launch_lmhead_fp8(const LmHeadFp8Launch& a, hipStream_t s) {
   g.tiles_n = (a.N + GBN - 1) / GBN;
   const int n_vt = (a.V + GBM - 1) / GBM;
   g.tiles_m = n_vt;
-  EpiLse e{a.partial, a.su, a.sw};
+  EpiLse e{a.partial, a.target, a.ids, a.su, a.sw};
   hipLaunchKernelGGL(gemm_tn_fp8<EpiLse>, dim3(n_vt * g.tiles_n), dim3(GNT), 0, s, g, e);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
-  hipLaunchKernelGGL(target_logit_fp8, dim3((a.N + 3) / 4), dim3(256), 0, s, a.uq, a.wq, a.su,
-                     a.sw, a.ids, a.target, a.N, a.D);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   hipLaunchKernelGGL(lse_combine, dim3((a.N + CMB_E - 1) / CMB_E), dim3(CMB_E * CMB_G), 0, s,
                      a.partial, n_vt, a.target, a.cu_d, a.n_seqs, a.n_frozen, a.N, a.scores,

@@ -1,8 +1,8 @@
 """Turn two rocprofv3 counter runs of `bench.py --pmc-driver` into HBM bytes per LM-head launch.
 
-    rocprofv3 --pmc FETCH_SIZE -d <dir_fetch> -o run --output-format csv -- python bench.py --pmc-driver
-    rocprofv3 --pmc WRITE_SIZE -d <dir_write> -o run --output-format csv -- python bench.py --pmc-driver
-    python -m paper_2607_27600_amd.pmc_summary <dir_fetch> <dir_write> profiles/lmhead_c2_traffic.json
+    rocprofv3 --pmc FETCH_SIZE -d <dir_fetch> -o run --output-format csv -- python bench.py --config C5 --pmc-driver
+    rocprofv3 --pmc WRITE_SIZE -d <dir_write> -o run --output-format csv -- python bench.py --config C5 --pmc-driver
+    python -m paper_2607_27600_amd.pmc_summary <dir_fetch> <dir_write> profiles/lmhead_c5_traffic.json C5
 
 A third mode tabulates matrix-core utilisation per kernel from one run with the SQ/GRBM
 counters named in util():
@@ -44,7 +44,7 @@ def _find(rows, pred):
     return hits
 
 
-def main(fetch_dir: str, write_dir: str, out: str) -> None:
+def main(fetch_dir: str, write_dir: str, out: str, cfg_name: str = "C5") -> None:
     f_rows = _per_dispatch(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
     w_rows = _per_dispatch(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
     is_lm = lambda n: "gemm_lmhead_packed" in n
@@ -58,16 +58,23 @@ def main(fetch_dir: str, write_dir: str, out: str) -> None:
     here = os.path.dirname(os.path.abspath(__file__))
     with open(os.path.join(here, "csrc", "gemm.hip"), "rb") as fh:
         digest = hashlib.sha256(fh.read()).hexdigest()
+    sys.path.insert(0, os.path.dirname(here))
+    from synth import configs as C
+    cfg = C.CONFIGS[cfg_name]
+    N, D, V = cfg.n_tokens, cfg.hidden, cfg.vocab
+    vt = (V + 255) // 256
+    alg = 2 * V * D + 2 * N * D + 8 * vt * N + 4 * N
     rec = {
-        "kernel": "gemm_lmhead_packed<EpiLse16> (LM head on packed operands + fused "
-                  "log-sum-exp), C2 shapes",
+        "kernel": f"gemm_lmhead_packed<EpiLse16> (LM head on packed operands + fused "
+                  f"log-sum-exp and target gather), {cfg_name} shapes",
         "fetch_kib_raw": f_lm, "write_kib_raw": w_lm,
         "copy_fetch_kib_raw": f_copy, "copy_write_kib_raw": w_copy,
         "fetch_scale": kf, "write_scale": kw,
         "bytes_per_launch": (f_lm * kf + w_lm * kw) * 1024.0,
-        "algorithmic_bytes": "W_lm 128256x4096 bf16 (1.05 GB) + U 4096x4096 bf16 (33.6 MB) read "
-                             "(both packed), "
-                             "partials 501x4096x8 B (16.4 MB) written",
+        "algorithmic_bytes": alg,
+        "algorithmic_bytes_note": f"W_lm {V}x{D} bf16 + U {N}x{D} bf16 read (both packed) + "
+                                  f"partials {vt}x{N}x8 B and target logits {N}x4 B written",
+        "traffic_over_algorithmic": (f_lm * kf + w_lm * kw) * 1024.0 / alg,
         "gemm_source_sha256": digest,
     }
     with open(out, "w") as fh:
@@ -115,4 +122,4 @@ if __name__ == "__main__":
     if sys.argv[1] == "util":
         util(sys.argv[2])
     else:
-        main(*sys.argv[1:4])
+        main(*sys.argv[1:5])

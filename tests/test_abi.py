@@ -220,11 +220,11 @@ def test_packed_lmhead_entry_points_validate_on_the_host():
     assert lib.cc_score_workspace(ctypes.byref(p2), ctypes.byref(n)) == cc.CC_ERR_ARG
     # the packed sub-step needs a packed problem and weight; the row-major one refuses it
     ws = ctypes.c_void_p(0x100000)
-    assert lib.cc_lmhead_score_packed(ctypes.byref(p0), dummy, dummy, dummy, dummy, dummy, None,
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p0), dummy, dummy, dummy, dummy, None,
                                       ws, big, None) == cc.CC_ERR_ARG
-    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, dummy, None, dummy, dummy, None,
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, None, dummy, dummy, None,
                                       ws, big, None) == cc.CC_ERR_ARG
-    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, dummy, odd, dummy, dummy, None,
+    assert lib.cc_lmhead_score_packed(ctypes.byref(p), dummy, odd, dummy, dummy, None,
                                       ws, big, None) == cc.CC_ERR_ARG
     assert lib.cc_lmhead_score(ctypes.byref(p), dummy, dummy, dummy, dummy, None, ws, big,
                                None) == cc.CC_ERR_ARG

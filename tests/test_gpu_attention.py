@@ -1,17 +1,19 @@
 """GPU parity of counter-causal attention (cc_attention_cc) against the oracle.
 
 Sizes span several 64-key tiles and 128-row blocks with ragged tails; GQA groups of
-1, 2, 4 and 7; contiguous and paged caches; both mask diagonals; the full-size
-Llama-3-8B shape on sampled rows.  Tolerance for bf16 outputs: the probabilities enter
-the second product rounded to bf16 and the output is stored in bf16, each a relative
-2^-9 error, so |o - ref| <= 2e-2 + 1e-2 |ref|; fp32 outputs agree within 1e-5."""
+1, 2, 4 and 7; head_dim 128 and 64; contiguous and paged caches; both mask diagonals;
+the full-size Llama-3-8B shapes on sampled rows at n = 4096 and n = 32768, and the
+Qwen2.5-7B ragged paged batch.  Tolerance for bf16 outputs: the stated
+|o - ref| <= 2e-2 + 1e-2 |ref|, and the per-row bar of tests/gpu_util.py
+(2^-8 |ref| + 2^-6 rms of the row's outputs), which a 10% error fails on rows that attend
+to thousands of keys; fp32 outputs agree within 1e-5."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import cc_oracle as O
 from synth import configs as C
-from tests.gpu_util import f64
+from tests.gpu_util import assert_attention_close, f64
 
 pytestmark = pytest.mark.gpu
 
@@ -42,10 +44,10 @@ def _run(cfg, diag="strict", rows=None):
     return got[rows], ref, rows
 
 
-def _check(got, ref, dtype):
+def _check(got, ref, dtype, what=""):
     assert np.all(np.isfinite(got))
     if dtype == "bf16":
-        np.testing.assert_allclose(got, ref, rtol=1e-2, atol=2e-2)
+        print(what, assert_attention_close(got, ref, what), flush=True)
     else:
         np.testing.assert_allclose(got, ref, rtol=0, atol=1e-5)
 
@@ -88,18 +90,54 @@ def test_bf16_mha_and_gqa2():
         _check(got, ref, "bf16")
 
 
+@pytest.mark.parametrize("diag", ["strict", "inclusive"])
+def test_bf16_head_dim_64_ragged_tail(diag):
+    cfg = C.shrink(C.C2, seq_lens=(300,), head_dim=64, cache_layers=1)
+    got, ref, _ = _run(cfg, diag)
+    _check(got, ref, "bf16", f"d=64 {diag}")
+    if diag == "strict":
+        assert np.all(got[-1] == 0)
+
+
+def test_bf16_head_dim_64_ragged_batch_gqa7():
+    cfg = C.shrink(C.C5, seq_lens=(1, 2, 63, 64, 65, 200), head_dim=64, paged=False,
+                   cache_layers=1, keep=(1, 1, 1, 1, 1, 1))
+    got, ref, _ = _run(cfg)
+    _check(got, ref, "bf16", "d=64 gqa7")
+
+
+def test_bf16_head_dim_64_paged_and_mha():
+    cfg = C.shrink(C.C5, seq_lens=(17, 100, 260, 16), head_dim=64, cache_layers=1,
+                   keep=(1, 1, 1, 1))
+    got, ref, _ = _run(cfg)
+    _check(got, ref, "bf16", "d=64 paged")
+    cfg = C.shrink(C.C2, seq_lens=(130, 70), head_dim=64, n_heads_q=4, n_heads_kv=4,
+                   cache_layers=1, keep=(1, 1))
+    got, ref, _ = _run(cfg)
+    _check(got, ref, "bf16", "d=64 mha")
+
+
 @pytest.mark.slow
 def test_c2_full_size_sampled_rows():
     rows = C.sample_rows(C.C2, count=96)
     got, ref, _ = _run(C.C2, rows=rows)
-    _check(got, ref, "bf16")
+    _check(got, ref, "bf16", "C2")
+
+
+@pytest.mark.slow
+def test_c3_full_length_sampled_rows():
+    """n = 32768 (Llama-3-8B shapes, 32 query / 8 KV heads): rows spread over the whole
+    sequence, most of them attending to tens of thousands of keys."""
+    rows = np.union1d(C.sample_rows(C.C3, count=48), [1000, 8000, 16000, 24000, 32000])
+    got, ref, _ = _run(C.C3, rows=rows)
+    _check(got, ref, "bf16", "C3")
 
 
 @pytest.mark.slow
 def test_c5_full_size_paged_sampled_rows():
     rows = C.sample_rows(C.C5, count=64)
     got, ref, _ = _run(C.C5, rows=rows)
-    _check(got, ref, "bf16")
+    _check(got, ref, "bf16", "C5")
 
 
 def test_bf16_outlier_key_channels():

@@ -51,28 +51,28 @@ def _fused_case(cfg, rows=None):
     cc.cc_score(p, inp, scores)
     torch.cuda.synchronize()
     h = w.host
-    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
-                              cfg.cu_seqlens, rows=rows)
+    ref, spread = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                                      cfg.cu_seqlens, rows=rows, spread=True)
     got = scores.cpu().numpy()
-    return (got if rows is None else got[rows]), ref
+    return (got if rows is None else got[rows]), ref, spread
 
 
 def test_fused_scores_c1_fp32():
-    got, ref = _fused_case(C.C1)
+    got, ref, _ = _fused_case(C.C1)
     print("C1 fused", assert_scores_close(got, ref, "f32", "C1 fused"))
 
 
 def test_fused_scores_bf16_small():
     cfg = C.shrink(C.C2, seq_lens=(300,), hidden=256, vocab=1000, cache_layers=1)
-    got, ref = _fused_case(cfg)
-    print("bf16 fused", assert_scores_close(got, ref, "bf16", "bf16-small fused"))
+    got, ref, spread = _fused_case(cfg)
+    print("bf16 fused", assert_scores_close(got, ref, "bf16", "bf16-small fused", spread))
 
 
 def test_fused_scores_bf16_paged_ragged():
     cfg = C.shrink(C.C5, seq_lens=(33, 1, 150, 64), hidden=512, vocab=3000, cache_layers=1,
                    keep=(1, 1, 1, 1))
-    got, ref = _fused_case(cfg)
-    print("paged fused", assert_scores_close(got, ref, "bf16", "paged-small fused"))
+    got, ref, spread = _fused_case(cfg)
+    print("paged fused", assert_scores_close(got, ref, "bf16", "paged-small fused", spread))
 
 
 def test_two_step_mode_requires_w_o():
@@ -90,5 +90,5 @@ def test_two_step_mode_requires_w_o():
 @pytest.mark.slow
 def test_fused_scores_c2_sampled():
     rows = C.sample_rows(C.C2, count=48)
-    got, ref = _fused_case(C.C2, rows=rows)
-    print("C2 fused", assert_scores_close(got, ref, "bf16", "C2 fused"))
+    got, ref, spread = _fused_case(C.C2, rows=rows)
+    print("C2 fused", assert_scores_close(got, ref, "bf16", "C2 fused", spread))

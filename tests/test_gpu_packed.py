@@ -60,7 +60,7 @@ def _lmhead_case(lens, D, V, n_frozen, seed):
                    head_dim=128, hidden=D, vocab=V, n_frozen=n_frozen, lmhead_packed=True)
     scores = torch.full((N,), float("nan"), dtype=torch.float32, device="cuda")
     lse = torch.empty(N, dtype=torch.float32, device="cuda")
-    cc.cc_lmhead_score_packed(p, dev(u), wd, wp, dev(ids), scores, lse)
+    cc.cc_lmhead_score_packed(p, dev(u), wp, dev(ids), scores, lse)
     # the row-major kernel on the same inputs, for the summation-order comparison
     p0 = cc.problem(dtype="bf16", cu_seqlens=cu.tolist(), n_heads_q=1, n_heads_kv=1,
                     head_dim=128, hidden=D, vocab=V, n_frozen=n_frozen)
@@ -99,8 +99,8 @@ def test_packed_score_two_step_and_fused():
     cfg = C.shrink(C.C2, seq_lens=(300, 45), hidden=256, vocab=1000, cache_layers=1)
     w = Workload(cfg, cache_layers=1, keep_host=True)
     h = w.host
-    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
-                              cfg.cu_seqlens)
+    ref, spread = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                                      cfg.cu_seqlens, spread=True)
     for mode in ("last_layer", "last_layer_fused"):
         print(f"[packed score] {mode}", flush=True)
         p = cc.problem(dtype="bf16", cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=cfg.n_heads_q,
@@ -112,7 +112,8 @@ def test_packed_score_two_step_and_fused():
         scores = torch.full((cfg.n_tokens,), float("nan"), dtype=torch.float32, device="cuda")
         cc.cc_score(p, inp, scores)
         torch.cuda.synchronize()
-        print(mode, assert_scores_close(scores.cpu().numpy(), ref, "bf16", f"packed {mode}"))
+        print(mode, assert_scores_close(scores.cpu().numpy(), ref, "bf16", f"packed {mode}",
+                                        spread))
         # without the packed weight the call is refused before anything runs
         inp0 = cc.inputs(kv=w.kv, token_ids=w.ids, w_lm=wl, q=w.q, w_o=w.w_o)
         with pytest.raises(cc.CCError):
@@ -128,7 +129,7 @@ def test_packed_zero_head_gives_ln_vocab():
     p = cc.problem(dtype="bf16", cu_seqlens=[0, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
                    hidden=D, vocab=V, lmhead_packed=True)
     scores = torch.empty(N, dtype=torch.float32, device="cuda")
-    cc.cc_lmhead_score_packed(p, dev(u), w, cc.cc_pack_lmhead(w), ids, scores)
+    cc.cc_lmhead_score_packed(p, dev(u), cc.cc_pack_lmhead(w), ids, scores)
     torch.cuda.synchronize()
     s = scores.cpu().numpy().astype(np.float64)
     assert s[-1] == np.inf
@@ -151,7 +152,7 @@ def test_packed_lmhead_c2_shape_sampled():
     p = cc.problem(dtype="bf16", cu_seqlens=[0, N], n_heads_q=1, n_heads_kv=1, head_dim=128,
                    hidden=D, vocab=V, lmhead_packed=True)
     scores = torch.empty(N, dtype=torch.float32, device="cuda")
-    cc.cc_lmhead_score_packed(p, dev(u), wd, wp, dev(ids), scores)
+    cc.cc_lmhead_score_packed(p, dev(u), wp, dev(ids), scores)
     torch.cuda.synchronize()
     rows = C.sample_rows(cfg, count=48)
     s_ref, _, _ = O.surprise(O.f64(u[rows]), w, ids[rows])

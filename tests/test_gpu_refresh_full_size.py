@@ -1,7 +1,8 @@
 """Whole refreshes at the full workload sizes, in the launch configuration the benchmark
 uses: scores on sampled rows against the oracle (rows are independent, so each sampled
-row is exact on its own), keep lists bit-exact against the oracle's selection on the
-GPU's own scores, and compaction checked byte for byte on sampled cache planes.
+row is exact on its own; the fast-variant scores also meet the spread bar of
+tests/gpu_util.py), keep lists bit-exact against the oracle's selection on the GPU's own
+scores, and compaction checked byte for byte on sampled cache planes.
 
   C3  n = 32768, Llama-3-8B shapes, keep 4096 per KV head, 32-layer cache in place
   C5  8 ragged sequences (2048..16384), Qwen2.5-7B shapes, paged P=16 pool, keep 20%
@@ -74,9 +75,10 @@ def test_c3_long_context_refresh():
     torch.cuda.synchronize()
     rows = C.sample_rows(cfg, count=48)
     h = w.host
-    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
-                              cfg.cu_seqlens, rows=rows)
-    print("[C3] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C3"))
+    ref, spread = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                                      cfg.cu_seqlens, rows=rows, spread=True)
+    print("[C3] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C3",
+                                             spread))
     keep, ks, lists = _select_and_check(w, scores, per_head=True)
     for hh in range(1, cfg.n_heads_kv):
         np.testing.assert_array_equal(lists[hh], lists[0])
@@ -99,9 +101,10 @@ def test_c5_ragged_paged_refresh():
     torch.cuda.synchronize()
     rows = C.sample_rows(cfg, count=64)
     h = w.host
-    ref = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
-                              cfg.cu_seqlens, rows=rows)
-    print("[C5] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C5"))
+    ref, spread = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
+                                      cfg.cu_seqlens, rows=rows, spread=True)
+    print("[C5] scores", assert_scores_close(scores.cpu().numpy()[rows], ref, "bf16", "C5",
+                                             spread))
     keep, ks, lists = _select_and_check(w, scores, per_head=False)
     k_before = bf16_host(w.k_cache)
     cc.cc_compact_kv(w.problem, w.kv, keep, ks, 0, w.ids)
