@@ -50,7 +50,9 @@ typedef enum cc_status {
   CC_ERR_DTYPE = 3,        /* dtype not valid for this call */
   CC_ERR_WORKSPACE = 4,    /* workspace smaller than the query returned */
   CC_ERR_UNSUPPORTED = 5,  /* a valid problem this build has no kernel for */
-  CC_ERR_HIP = 6           /* the HIP runtime rejected a launch or copy */
+  CC_ERR_HIP = 6,          /* the HIP runtime rejected a launch or copy */
+  CC_ERR_SCRATCH = 7       /* the call needs more than the static scratch of the
+                              allocation-free entry point holds */
 } cc_status;
 
 typedef enum cc_dtype { CC_F32 = 0, CC_BF16 = 1 } cc_dtype;
@@ -212,6 +214,25 @@ cc_status cc_lmhead_workspace(const cc_problem* p, size_t* bytes);
 cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
                           const int32_t* token_ids, float* scores, float* lse,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the static device scratch behind cc_lmhead_score_noalloc (per GPU). */
+#define CC_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* cc_lmhead_score without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Arguments, results and errors are those of cc_lmhead_score with p->lmhead_packed = 0
+ * (a packed problem returns CC_ERR_ARG); the scratch that cc_lmhead_workspace(p) would
+ * size -- the per-(vocabulary tile, entry) log-sum-exp partials and the target logits,
+ * written in full by every call -- lives in a static device array of
+ * CC_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until the process
+ * ends.  A problem whose cc_lmhead_workspace exceeds it returns CC_ERR_SCRATCH before
+ * anything is enqueued (32 MiB covers, e.g., 4096 entries of a 128256-word vocabulary:
+ * about 8 B per entry per 256 words).  The call allocates nothing.  Every call on one GPU
+ * shares that GPU's array: calls whose execution overlaps on one GPU (two streams, or two
+ * host threads) race and must be ordered by the caller. */
+cc_status cc_lmhead_score_noalloc(const cc_problem* p, const void* u, const void* w_lm,
+                                  const int32_t* token_ids, float* scores, float* lse,
+                                  void* stream);
 
 /* Workspace for cc_fuse_wo_lmhead: the transposed W_o. */
 cc_status cc_fuse_wo_lmhead_workspace(int32_t dtype, int32_t hidden, int32_t qdim,

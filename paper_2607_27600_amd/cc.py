@@ -18,7 +18,9 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcc.so")
 
-CC_OK, CC_ERR_ARG, CC_ERR_SHAPE, CC_ERR_DTYPE, CC_ERR_WORKSPACE, CC_ERR_UNSUPPORTED, CC_ERR_HIP = range(7)
+(CC_OK, CC_ERR_ARG, CC_ERR_SHAPE, CC_ERR_DTYPE, CC_ERR_WORKSPACE, CC_ERR_UNSUPPORTED, CC_ERR_HIP,
+ CC_ERR_SCRATCH) = range(8)
+CC_NOALLOC_SCRATCH_BYTES = 32 << 20
 CC_F32, CC_BF16 = 0, 1
 CC_DIAG_STRICT, CC_DIAG_INCLUSIVE = 0, 1
 CC_MODE_LAST_LAYER, CC_MODE_FULL, CC_MODE_LAST_LAYER_H, CC_MODE_LAST_LAYER_FUSED = 0, 1, 2, 3
@@ -31,7 +33,7 @@ EXPORTED = [
     "cc_compact_rows_workspace", "cc_compact_rows", "cc_fuse_wo_lmhead_workspace",
     "cc_fuse_wo_lmhead", "cc_quantize_fp8_workspace", "cc_quantize_fp8",
     "cc_lmhead_fp8_workspace", "cc_lmhead_score_fp8", "cc_pack_lmhead_bytes", "cc_pack_lmhead",
-    "cc_lmhead_score_packed",
+    "cc_lmhead_score_packed", "cc_lmhead_score_noalloc",
 ]
 
 _c_void_p = ctypes.c_void_p
@@ -87,6 +89,8 @@ def _load():
         "cc_lmhead_workspace": (st, [P(c_problem), sz]),
         "cc_lmhead_score": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                  _c_void_p, _c_void_p, ctypes.c_size_t, _c_void_p]),
+        "cc_lmhead_score_noalloc": (st, [P(c_problem), _c_void_p, _c_void_p, _c_void_p,
+                                         _c_void_p, _c_void_p, _c_void_p]),
         "cc_linear": (st, [_i32, _c_void_p, _c_void_p, _c_void_p, _i32, _i32, _i32, _c_void_p]),
         "cc_fuse_wo_lmhead_workspace": (st, [_i32, _i32, _i32, sz]),
         "cc_quantize_fp8_workspace": (st, [_i64, sz]),
@@ -318,6 +322,16 @@ def cc_lmhead_score(p: Problem, u: torch.Tensor, w_lm: torch.Tensor, token_ids: 
     _check(_lib.cc_lmhead_score(ctypes.byref(p.struct), _ptr(u), _ptr(w_lm), _ptr(token_ids),
                                 _ptr(scores), _ptr(lse), _ptr(workspace), workspace.numel(),
                                 _stream(stream)), "cc_lmhead_score")
+    return scores
+
+
+def cc_lmhead_score_noalloc(p: Problem, u: torch.Tensor, w_lm: torch.Tensor,
+                            token_ids: torch.Tensor, scores: torch.Tensor,
+                            lse: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """cc_lmhead_score with its scratch in the library's static device array (no workspace)."""
+    _check(_lib.cc_lmhead_score_noalloc(ctypes.byref(p.struct), _ptr(u), _ptr(w_lm),
+                                        _ptr(token_ids), _ptr(scores), _ptr(lse),
+                                        _stream(stream)), "cc_lmhead_score_noalloc")
     return scores
 
 

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "cc_internal.h"
@@ -420,6 +421,7 @@ const char* cc_status_str(cc_status s) {
     case CC_ERR_WORKSPACE: return "CC_ERR_WORKSPACE: workspace too small";
     case CC_ERR_UNSUPPORTED: return "CC_ERR_UNSUPPORTED: no kernel for this shape";
     case CC_ERR_HIP: return "CC_ERR_HIP: HIP runtime error";
+    case CC_ERR_SCRATCH: return "CC_ERR_SCRATCH: larger than the static scratch of the allocation-free entry point";
   }
   return "unknown cc_status";
 }
@@ -459,6 +461,53 @@ cc_status cc_lmhead_score(const cc_problem* p, const void* u, const void* w_lm,
   if (p->dtype == CC_BF16 && (!aligned16(u) || !aligned16(w_lm))) return CC_ERR_ARG;
   if (p->lmhead_packed && n_tokens(p) > 0) return CC_ERR_ARG;   // cc_lmhead_score_packed
   CC_TRY(check_ws(ws, ws_bytes, lmhead_ws_bytes(p)));
+  return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ allocation-free LM head
+// The scratch of cc_lmhead_score_noalloc: a file-scope device array, one per GPU.  In host
+// code its name is a host-side stand-in, not a device address, so it is never passed to a
+// kernel or a copy; the device address comes from hipGetSymbolAddress, taken once per
+// device with that device current and kept here.
+namespace {
+static __device__ __align__(256) unsigned char scratch[CC_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch's device address on the current device (looked up on its first use there).
+cc_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return CC_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return CC_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return CC_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CC_OK;
+}
+}  // namespace
+
+extern "C" {
+
+cc_status cc_lmhead_score_noalloc(const cc_problem* p, const void* u, const void* w_lm,
+                                  const int32_t* token_ids, float* scores, float* lse,
+                                  void* stream) {
+  CC_TRY(check_problem(p));
+  if (p->lmhead_packed) return CC_ERR_ARG;
+  if (n_tokens(p) > 0 && (!u || !w_lm || !token_ids || !scores)) return CC_ERR_ARG;
+  if (p->dtype == CC_BF16 && (!aligned16(u) || !aligned16(w_lm))) return CC_ERR_ARG;
+  const size_t need = lmhead_ws_bytes(p);
+  if (need > CC_NOALLOC_SCRATCH_BYTES) return CC_ERR_SCRATCH;
+  if (n_tokens(p) == 0) return CC_OK;
+  void* ws = nullptr;
+  CC_TRY(scratch_address(&ws));
   return run_lmhead(p, u, w_lm, token_ids, scores, lse, ws, static_cast<hipStream_t>(stream));
 }
 
