@@ -422,9 +422,14 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
                       "ms": part["compact"], "gb_s": cmp_bytes / (part["compact"] * 1e-3) / 1e9,
                       "frac_hbm": cmp_bytes / (part["compact"] * 1e-3) / 1e9 / PEAK_HBM_GBS}
 
-    # in-place compaction (what a live refresh does), with and without the cache flushed;
-    # every call reads and writes the same rows
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    if with_extras:
+        res["select_sweep"] = select_sweep(dev, flush)
+    if with_extras and not full:
+        res.update(next4_extras(args, cc, w, p, cfg, o, u, scores, ks, starts, lens, ws_att,
+                                ws_sel, ws_cmp, out_kv, stream, ms_step, part["lmhead_lse"]))
+    # in-place compaction (what a live refresh does), with and without the cache flushed;
+    # every call reads and writes the same rows.  Last: it rewrites the workload's cache.
     cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp)
     ev_ip = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
@@ -441,13 +446,7 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
                                "ms_cache_flushed": ip_fl,
                                "gb_s_cache_flushed": cmp_bytes / (ip_fl * 1e-3) / 1e9,
                                "frac_hbm_cache_flushed": cmp_bytes / (ip_fl * 1e-3) / 1e9 / PEAK_HBM_GBS}
-    if with_extras:
-        res["select_sweep"] = select_sweep(dev, flush)
-    del flush
-    if with_extras and not full:
-        res.update(next4_extras(args, cc, w, p, cfg, o, u, scores, ks, starts, lens, ws_att,
-                                ws_sel, ws_cmp, out_kv, stream, ms_step, part["lmhead_lse"]))
-    del out_kv
+    del flush, out_kv
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, CPU_ROWS.get(name, 64))
     return res
