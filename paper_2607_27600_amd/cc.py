@@ -13,6 +13,7 @@ import os
 from dataclasses import dataclass, field
 from typing import Optional, Sequence
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -435,17 +436,27 @@ def cc_select_workspace(n_segs: int) -> int:
     return _query(_lib.cc_select_workspace, n_segs)
 
 
+def _host_array(x, dtype):
+    """A C-contiguous numpy array of the given integer type (no copy if it is one)."""
+    return np.ascontiguousarray(np.asarray(x), dtype=dtype)
+
+
 def cc_select_keep(scores: torch.Tensor, seg_start: Sequence[int], seg_len: Sequence[int],
                    k: Sequence[int], keep_idx: torch.Tensor,
                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    n = len(seg_len)
-    st = (_i64 * n)(*[int(x) for x in seg_start])
-    ln = (_i32 * n)(*[int(x) for x in seg_len])
-    kk = (_i32 * n)(*[int(x) for x in k])
+    """seg_start, seg_len, k: host sequences or numpy arrays (int64, int32, int32 arrays
+    are passed without a copy)."""
+    st = _host_array(seg_start, np.int64)
+    ln = _host_array(seg_len, np.int32)
+    kk = _host_array(k, np.int32)
+    n = len(ln)
     if workspace is None:
         workspace = _workspace(cc_select_workspace(n), scores.device)
-    _check(_lib.cc_select_keep(_ptr(scores), n, st, ln, kk, _ptr(keep_idx), _ptr(workspace),
-                               workspace.numel(), _stream(stream)), "cc_select_keep")
+    _check(_lib.cc_select_keep(_ptr(scores), n, st.ctypes.data_as(ctypes.POINTER(_i64)),
+                               ln.ctypes.data_as(ctypes.POINTER(_i32)),
+                               kk.ctypes.data_as(ctypes.POINTER(_i32)), _ptr(keep_idx),
+                               _ptr(workspace), workspace.numel(), _stream(stream)),
+           "cc_select_keep")
     return keep_idx
 
 

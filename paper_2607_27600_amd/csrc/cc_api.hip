@@ -748,8 +748,9 @@ cc_status cc_select_keep(const float* scores, int32_t n_segs, const int64_t* seg
   if (any_len && (!scores || !keep_idx)) return CC_ERR_ARG;
   CC_TRY(check_ws(ws, ws_bytes, align_up(size_t(n_segs) * sizeof(SelSeg))));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // a few descriptors travel in the kernel arguments; more are copied into the workspace
-  if (n_segs > SEL_INLINE)
+  // a few descriptors travel in the kernel arguments, regular layouts as a formula; others
+  // are copied into the workspace
+  if (n_segs > SEL_INLINE && !select_regular(segs.data(), n_segs))
     CC_HIP(hipMemcpyAsync(ws, segs.data(), segs.size() * sizeof(SelSeg), hipMemcpyHostToDevice, s));
   CC_HIP(launch_select(scores, segs.data(), static_cast<const SelSeg*>(ws), n_segs, mx, keep_idx, s));
   return CC_OK;

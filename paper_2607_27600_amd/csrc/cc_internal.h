@@ -159,8 +159,14 @@ struct SelSeg {
 constexpr int SEL_INLINE = 16;
 struct SelInline {
   SelSeg s[SEL_INLINE];
-  int n;   // descriptors held here (0: all are read from the device table)
+  int n;        // descriptors held here (0: all are read from the device table)
+  int regular;  // 1: segment b is {start0 + b * stride, len, k, out b * k} (no table)
+  int64_t start0, stride;
+  int32_t len, k;
 };
+// True when the segments are equal (length and k) at a fixed start stride with outputs
+// back to back: their descriptors need no upload.
+bool select_regular(const SelSeg* segs_h, int n_segs);
 // segs_h: the descriptors on the host; segs_d: the same in device memory, read only when
 // n_segs > SEL_INLINE (may be null otherwise).
 hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg* segs_d,

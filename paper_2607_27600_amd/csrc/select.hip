@@ -9,6 +9,8 @@
 // ballot/prefix counts.  Integer work only: the result is exact.  Launches whose longest
 // segment holds 8193..32768 scores keep every segment in registers (one read of the
 // scores); the others re-read the scores from memory at every pass.
+#include <algorithm>
+
 #include "cc_internal.h"
 
 namespace cc {
@@ -16,6 +18,14 @@ namespace {
 
 constexpr int SNT = 1024;           // threads per segment
 constexpr int SWAVES = SNT / 64;
+
+// Descriptor of segment b: computed for regular launches, else by value in the kernel
+// arguments (the first SEL_INLINE) or from the uploaded table.
+__device__ __forceinline__ SelSeg seg_desc(const SelInline& inl, const SelSeg* segs, int b) {
+  if (inl.regular)
+    return SelSeg{inl.start0 + int64_t(b) * inl.stride, inl.len, inl.k, int64_t(b) * inl.k};
+  return b < inl.n ? inl.s[b] : segs[b];
+}
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
@@ -50,7 +60,7 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
   __shared__ uint32_t hist[256];
   __shared__ int wsum[SWAVES];
   __shared__ uint32_t sh_digit, sh_rem, sh_cnt;
-  const SelSeg sg = int(blockIdx.x) < inl.n ? inl.s[blockIdx.x] : segs[blockIdx.x];
+  const SelSeg sg = seg_desc(inl, segs, int(blockIdx.x));
   const float* s = scores + sg.start;
   int32_t* out = keep + sg.out;
   const int n = sg.len, k = sg.k;
@@ -140,14 +150,19 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
 //    the radix digits run on rel = key - kmin over the B = bit length of kmaxf - kmin
 //    bits, so the first digit spreads over the finite scores' actual range (the +inf of a
 //    sequence's last entry would otherwise squeeze them all into one bucket).
-//  - One 8-bit pass over every key (per-wave LDS histograms).  When the bucket that holds
-//    the threshold has at most CMAX keys, their low bits are copied to LDS and one wave
-//    finishes the lower digits on that list, with no further block-wide barriers;
-//    otherwise further block-wide passes run over the registers.
+//  - One 11-bit pass over every key into a 2048-bin LDS histogram.  An 11-bit digit leaves
+//    about an eighth of the keys an 8-bit one would in the bucket that holds the threshold,
+//    and spreads a wave's atomics over more bins, so fewer lanes of one instruction
+//    collide.  When that bucket has at most CMAX keys, their low bits are copied to LDS and
+//    one wave finishes the lower digits on that list (9 bits a pass, no block-wide
+//    barrier); otherwise further 11-bit block-wide passes run over the registers.
+//  - Bucket searches are two-level wave scans: lane sums over the lanes' bin ranges, then
+//    the bins of the lane that holds the rank.
 //  - Emission: a thread's flagged keys per chunk are counted, and one batched scan over
 //    the workgroup (8 chunk counts per thread, two per word) gives every flagged key its
 //    rank in index order: first for the ties (when not all of them are kept), then for
-//    the kept keys, which are written at their ranks.
+//    the kept keys, which are staged in LDS at their ranks (8192 at a time) and written
+//    out as consecutive words.
 constexpr int RNT = 1024;
 constexpr int RWAVES = RNT / 64;
 constexpr int RCW = 4;                 // scores per thread per chunk
@@ -155,53 +170,65 @@ constexpr int RCH = 8;                 // chunks
 constexpr int RCHUNK = RNT * RCW;      // scores per chunk
 constexpr int RPT = RCH * RCW;         // scores per thread
 constexpr int RMAX = RNT * RPT;
-constexpr int CMAX = 4096;
+constexpr int CMAX = 4096;             // candidate list of the one-wave finish
 constexpr uint32_t KINF = 0xff800000u;   // order_key(+inf): the largest key
+constexpr int SD = 11;                 // bits of a block-wide digit
+constexpr int SBINS = 1 << SD;
+constexpr int WD = 9;                  // bits of a digit of the one-wave finish
+constexpr int WBINS = 1 << WD;
+constexpr int OWIN = 8192;             // kept indices staged in LDS per window
 
 struct Pick {
   uint32_t digit, rem, cnt;
 };
 
-// Run by one whole wave: in a 256-bin histogram searched from the highest digit down, the
-// bin holding the rem-th largest counted key (1 <= rem <= total), the rank left inside it
-// and its count; every lane receives the result.
-__device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int lane) {
-  // lane l owns digits 255-4l .. 252-4l (descending)
-  uint32_t c[4], sum = 0u;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    c[q] = h[255 - 4 * lane - q];
-    sum += c[q];
-  }
-  uint32_t incl = sum;
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t t = __shfl_up(incl, off);
-    if (lane >= off) incl += t;
+    const uint32_t t = uint32_t(__shfl_up(int(x), off));
+    if (lane >= off) x += t;
   }
-  const uint32_t excl = incl - sum;
-  const bool mine = excl < rem && incl >= rem;
-  uint32_t digit = 0u, r = 0u, cn = 0u, acc = excl;
-  bool done = false;
+  return x;
+}
+
+// Run by one whole wave: in a histogram of 64 * BPL bins searched from the highest bin down,
+// the bin holding the rem-th largest counted key (1 <= rem <= total), the rank left inside
+// it and its count; every lane receives the result.  Level 1: lane l sums bins
+// 64 BPL - BPL (l + 1) .. 64 BPL - 1 - BPL l and a wave scan finds the lane whose range
+// holds the rank; level 2: lane j < BPL reads that range's j-th highest bin and a second
+// scan finds the bin.
+template <int BPL>
+__device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int lane) {
+  constexpr int NB = 64 * BPL;
+  const uint32_t* mine = h + NB - BPL * (lane + 1);
+  uint32_t sum = 0u;
+  if constexpr (BPL % 4 == 0) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    if (mine && !done && acc + c[q] >= rem) {
-      digit = uint32_t(255 - 4 * lane - q);
-      r = rem - acc;
-      cn = c[q];
-      done = true;
+    for (int q = 0; q < BPL / 4; ++q) {
+      const uint4 v = reinterpret_cast<const uint4*>(mine)[q];
+      sum += (v.x + v.y) + (v.z + v.w);
     }
-    acc += c[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < BPL; ++q) sum += mine[q];
   }
-  const uint64_t bal = __ballot(mine);
-  const int src = bal ? __builtin_ctzll(bal) : 0;
-  return {uint32_t(__shfl(int(digit), src)), uint32_t(__shfl(int(r), src)),
-          uint32_t(__shfl(int(cn), src))};
+  const uint32_t incl = wave_incl_scan(sum, lane);
+  const uint64_t over = __ballot(incl >= rem);
+  const int owner = over ? int(__builtin_ctzll(over)) : 63;   // rem <= total: some lane does
+  const uint32_t before = uint32_t(__shfl(int(incl - sum), owner));
+  const int top = NB - BPL * owner - 1;              // the owner's highest bin
+  const uint32_t c = lane < BPL ? h[top - lane] : 0u;
+  const uint32_t incl2 = wave_incl_scan(c, lane);
+  const uint64_t hit = __ballot(lane < BPL && before + incl2 >= rem);
+  const int j = hit ? int(__builtin_ctzll(hit)) : BPL - 1;
+  const uint32_t cj = uint32_t(__shfl(int(c), j));
+  const uint32_t ij = uint32_t(__shfl(int(incl2), j));
+  return {uint32_t(top - j), rem - before - (ij - cj), cj};
 }
 
 // Ranks in index order of the keys flagged in m (bit 4c + i: slot i of chunk c): base[c]
 // = flagged keys before this thread's part of chunk c.  wtot: [RWAVES][RCH / 2] words of
-// LDS owned by this call.  Contains one barrier.
+// LDS owned by this call (16-byte aligned rows).  Contains one barrier.
 static_assert(RPT == 32, "one bit per key in a 32-bit mask");
 __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
                                               uint32_t (*wtot)[RCH / 2], int lane, int wave) {
@@ -220,40 +247,46 @@ __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
       const uint32_t t = uint32_t(__shfl_up(int(inc[q]), off));
       if (lane >= off) inc[q] += t;
     }
-  if (lane == 63)
-#pragma unroll
-    for (int q = 0; q < RCH / 2; ++q) wtot[wave][q] = inc[q];
+  if (lane == 63) *reinterpret_cast<uint4*>(wtot[wave]) = make_uint4(inc[0], inc[1], inc[2], inc[3]);
   __syncthreads();
+  uint32_t all[RCH / 2] = {0u, 0u, 0u, 0u}, bef[RCH / 2] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int w = 0; w < RWAVES; ++w) {
+    const uint4 t = *reinterpret_cast<const uint4*>(wtot[w]);
+    const uint32_t tv[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int q = 0; q < RCH / 2; ++q) {
+      all[q] += tv[q];
+      bef[q] += w < wave ? tv[q] : 0u;
+    }
+  }
   uint32_t run = 0u;
 #pragma unroll
   for (int q = 0; q < RCH / 2; ++q) {
-    uint32_t all = 0u, before = 0u;
-#pragma unroll
-    for (int w = 0; w < RWAVES; ++w) {
-      const uint32_t t = wtot[w][q];
-      all += t;
-      before += w < wave ? t : 0u;
-    }
-    const uint32_t mine = before + inc[q] - own[q];
+    const uint32_t mine = bef[q] + inc[q] - own[q];
     base[2 * q] = run + (mine & 0xffffu);
-    run += all & 0xffffu;
+    run += all[q] & 0xffffu;
     base[2 * q + 1] = run + (mine >> 16);
-    run += all >> 16;
+    run += all[q] >> 16;
   }
 }
 
-__global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restrict__ scores,
+struct RegLds {
+  uint32_t hist[SBINS];
+  uint32_t cand[CMAX];
+  uint32_t whist[WBINS];
+  int32_t stg[OWIN];
+  uint32_t red[3][RWAVES];
+  __attribute__((aligned(16))) uint32_t wtot[2][RWAVES][RCH / 2];
+  uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
+};
+
+__global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restrict__ scores,
                                                            const SelSeg* __restrict__ segs,
                                                            SelInline inl,
                                                            int32_t* __restrict__ keep) {
-  __shared__ uint32_t hist[2][RWAVES][256];
-  __shared__ uint32_t tot[256];
-  __shared__ uint32_t cand[CMAX];
-  __shared__ uint32_t whist[256];
-  __shared__ uint32_t red[3][RWAVES];
-  __shared__ uint32_t wtot[2][RWAVES][RCH / 2];
-  __shared__ uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
-  const SelSeg sg = int(blockIdx.x) < inl.n ? inl.s[blockIdx.x] : segs[blockIdx.x];
+  __shared__ __attribute__((aligned(16))) RegLds L;
+  const SelSeg sg = seg_desc(inl, segs, int(blockIdx.x));
   const int n = sg.len, k = sg.k;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int32_t* out = keep + sg.out;
@@ -302,8 +335,7 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
   }
   auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
 
-  // extremes of the segment and its number of +inf keys; the first histogram buffer is
-  // cleared meanwhile
+  // extremes of the segment and its number of +inf keys; the histogram is cleared meanwhile
   uint32_t kmin = 0xffffffffu, kmaxf = 0u, ninf = 0u;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
@@ -319,21 +351,21 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
     ninf += uint32_t(__shfl_xor(int(ninf), off));
   }
   if (lane == 0) {
-    red[0][wave] = kmin;
-    red[1][wave] = kmaxf;
-    red[2][wave] = ninf;
+    L.red[0][wave] = kmin;
+    L.red[1][wave] = kmaxf;
+    L.red[2][wave] = ninf;
   }
-  for (int i = tid; i < RWAVES * 256; i += RNT) (&hist[0][0][0])[i] = 0u;
-  if (tid == 0) sh_ncand = 0u;
+  for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
+  if (tid == 0) L.sh_ncand = 0u;
   __syncthreads();
-  kmin = red[0][0];
-  kmaxf = red[1][0];
-  ninf = red[2][0];
+  kmin = L.red[0][0];
+  kmaxf = L.red[1][0];
+  ninf = L.red[2][0];
 #pragma unroll
   for (int w = 1; w < RWAVES; ++w) {
-    kmin = min(kmin, red[0][w]);
-    kmaxf = max(kmaxf, red[1][w]);
-    ninf += red[2][w];
+    kmin = min(kmin, L.red[0][w]);
+    kmaxf = max(kmaxf, L.red[1][w]);
+    ninf += L.red[2][w];
   }
   // From here on the registers hold rel = key - kmin: the order is unchanged and +inf
   // keys are the ones equal to rinf.  Padding (indices past the end) becomes rel 0, the
@@ -359,96 +391,89 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
     if (B == 0) {
       cnt = uint32_t(n) - ninf;   // every key below +inf equals kmin
     } else {
-      int hi = B, buf = 0;
+      int hi = B;
       bool first = true;
       while (hi > 0) {
-        const int lo = hi > 8 ? hi - 8 : 0;
+        const int lo = hi > SD ? hi - SD : 0;
         const uint32_t dmask = (1u << (hi - lo)) - 1u;
-        uint32_t(*h)[256] = hist[buf];
 #pragma unroll
         for (int j = 0; j < RPT; ++j) {
           const uint32_t rel = key[j];
           const uint32_t top = hi >= 32 ? 0u : rel >> hi;
-          if (rel != rinf && top == prefix) atomicAdd(&h[wave][(rel >> lo) & dmask], 1u);
-          __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 64 live masks
+          if (rel != rinf && top == prefix) atomicAdd(&L.hist[(rel >> lo) & dmask], 1u);
+          __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 32 live masks
         }
-        __syncthreads();
-        if (tid < 256) {
-          uint32_t t = 0u;
-#pragma unroll
-          for (int w = 0; w < RWAVES; ++w) t += h[w][tid];
-          tot[tid] = t;
-        }
-        for (int i = tid; i < RWAVES * 256; i += RNT) (&hist[buf ^ 1][0][0])[i] = 0u;
         __syncthreads();
         if (wave == 0) {
-          const Pick p = pick_bucket(tot, rem, lane);
+          const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
           if (lane == 0) {
-            sh_digit = p.digit;
-            sh_rem = p.rem;
-            sh_cnt = p.cnt;
+            L.sh_digit = p.digit;
+            L.sh_rem = p.rem;
+            L.sh_cnt = p.cnt;
           }
         }
         __syncthreads();
-        prefix = (prefix << (hi - lo)) | sh_digit;
-        rem = sh_rem;
-        cnt = sh_cnt;
+        prefix = (prefix << (hi - lo)) | L.sh_digit;
+        rem = L.sh_rem;
+        cnt = L.sh_cnt;
         hi = lo;
-        buf ^= 1;
-        if (first && hi > 0 && cnt <= uint32_t(CMAX)) {
+        const bool to_list = first && hi > 0 && cnt <= uint32_t(CMAX);
+        if (hi > 0 && !to_list) {
+          // another block-wide digit follows: clear the histogram (the pick above read it
+          // before the barrier that ended it)
+          for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
+          __syncthreads();
+        }
+        if (to_list) {
           // The `cnt` keys of the chosen bucket (rel >> hi == prefix) go to LDS as their
           // low hi bits, each thread's after those of the lanes before it.
-          const int L = hi;
-          const uint32_t lmask = (1u << L) - 1u;
+          const int Lb = hi;
+          const uint32_t lmask = (1u << Lb) - 1u;
           uint32_t cmask = 0u;
 #pragma unroll
-          for (int j = 0; j < RPT; ++j) cmask |= uint32_t(key[j] != rinf && (key[j] >> L) == prefix) << j;
+          for (int j = 0; j < RPT; ++j)
+            cmask |= uint32_t(key[j] != rinf && (key[j] >> Lb) == prefix) << j;
           const uint32_t mine = uint32_t(__popc(cmask));
-          uint32_t incl = mine;
-#pragma unroll
-          for (int off = 1; off < 64; off <<= 1) {
-            const uint32_t t = uint32_t(__shfl_up(int(incl), off));
-            if (lane >= off) incl += t;
-          }
+          const uint32_t incl = wave_incl_scan(mine, lane);
           uint32_t base = 0u;
-          if (lane == 63) base = atomicAdd(&sh_ncand, incl);
+          if (lane == 63) base = atomicAdd(&L.sh_ncand, incl);
           uint32_t pos = uint32_t(__shfl(int(base), 63)) + incl - mine;
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
             if ((cmask >> j) & 1u) {
-              if (pos < uint32_t(CMAX)) cand[pos] = key[j] & lmask;
+              if (pos < uint32_t(CMAX)) L.cand[pos] = key[j] & lmask;
               ++pos;
             }
             __builtin_amdgcn_sched_barrier(0);
           }
           __syncthreads();
           if (wave == 0) {
-            // radix passes of 8 bits over the list, by this wave alone: its LDS operations
+            // radix passes of WD bits over the list, by this wave alone: its LDS operations
             // execute in program order, so the clears, the atomics and the reads of whist
             // need no barrier (the waits and fences keep the compiler from moving them)
             const int nc = int(min(cnt, uint32_t(CMAX)));
             uint32_t p2 = 0u, r2 = rem, c2 = cnt;
-            int h2 = L;
+            int h2 = Lb;
             while (h2 > 0) {
-              const int l2 = h2 > 8 ? h2 - 8 : 0;
+              const int l2 = h2 > WD ? h2 - WD : 0;
               const uint32_t m2 = (1u << (h2 - l2)) - 1u;
 #pragma unroll
-              for (int q = 0; q < 4; ++q) whist[4 * lane + q] = 0u;
+              for (int q = 0; q < WBINS / 64; ++q) L.whist[WBINS / 64 * lane + q] = 0u;
               asm volatile("" ::: "memory");
               // eight reads in flight before their atomics: the list is walked at LDS
               // throughput rather than one read latency per element
               for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
                 uint32_t vv[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) vv[u] = cand[min(i0 + u * 64 + lane, CMAX - 1)];
+                for (int u = 0; u < 8; ++u) vv[u] = L.cand[min(i0 + u * 64 + lane, CMAX - 1)];
 #pragma unroll
                 for (int u = 0; u < 8; ++u)
                   if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
-                    atomicAdd(&whist[(vv[u] >> l2) & m2], 1u);
+                    atomicAdd(&L.whist[(vv[u] >> l2) & m2], 1u);
               }
               __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
               asm volatile("" ::: "memory");
-              const Pick pk = pick_bucket(whist, r2, lane);
+              const Pick pk = pick_bucket<WBINS / 64>(L.whist, r2, lane);
               __builtin_amdgcn_s_waitcnt(0xc07f);
               asm volatile("" ::: "memory");
               p2 = (p2 << (h2 - l2)) | pk.digit;
@@ -457,15 +482,15 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
               h2 = l2;
             }
             if (lane == 0) {
-              sh_digit = p2;
-              sh_rem = r2;
-              sh_cnt = c2;
+              L.sh_digit = p2;
+              L.sh_rem = r2;
+              L.sh_cnt = c2;
             }
           }
           __syncthreads();
-          prefix = (prefix << L) | sh_digit;
-          rem = sh_rem;
-          cnt = sh_cnt;
+          prefix = (prefix << Lb) | L.sh_digit;
+          rem = L.sh_rem;
+          cnt = L.sh_cnt;
           hi = 0;
         }
         first = false;
@@ -488,37 +513,49 @@ __global__ __launch_bounds__(RNT, 4) void select_keep_regs(const float* __restri
     take |= eq;
   } else {
     // ties ranked in index order; the first rem are kept
-    chunk_offsets(eq, base, wtot[0], lane, wave);
+    chunk_offsets(eq, base, L.wtot[0], lane, wave);
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
       const uint32_t below = uint32_t(__popc(eq & (((1u << (j & 3)) - 1u) << (j & ~3))));
       take |= uint32_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
     }
   }
-  chunk_offsets(take, base, wtot[1], lane, wave);
+  chunk_offsets(take, base, L.wtot[1], lane, wave);
   int t4s = 4 * tid;
   asm volatile("" : "+v"(t4s));
-  // A thread's kept keys of chunk c take consecutive ranks base[c], base[c] + 1, ...;
-  // store u writes each lane's u-th kept key of the chunk (consecutive lanes write mostly
-  // consecutive ranks), and is skipped when no lane of the wave has one.
+  // A thread's kept keys of chunk c take consecutive ranks base[c], base[c] + 1, ...: each
+  // is staged at its rank in LDS, OWIN ranks at a time, and the window leaves as
+  // consecutive words (one coalesced store per thread and 1024 indices).
+  for (int w0 = 0; w0 < k; w0 += OWIN) {
 #pragma unroll
-  for (int c = 0; c < RCH; ++c) {
-    uint32_t t = (take >> (RCW * c)) & 0xfu;
+    for (int c = 0; c < RCH; ++c) {
+      uint32_t r = base[c] - uint32_t(w0);
 #pragma unroll
-    for (int u = 0; u < RCW; ++u) {
-      if (!__any(t != 0u)) break;
-      if (t != 0u) {
-        const uint32_t pos = base[c] + uint32_t(u);
-        if (pos < uint32_t(k))   // pos < k always; bounds the store
-          out[pos] = c * RCHUNK + t4s + __builtin_ctz(t);
-        t &= t - 1u;
+      for (int u = 0; u < RCW; ++u) {
+        if ((take >> (RCW * c + u)) & 1u) {
+          if (r < uint32_t(OWIN)) L.stg[r] = c * RCHUNK + t4s + u;
+          ++r;
+        }
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    const int m = min(OWIN, k - w0);
+    for (int i = tid; i < m; i += RNT) out[w0 + i] = L.stg[i];
+    if (w0 + OWIN < k) __syncthreads();   // the next window reuses the staging area
   }
 }
 
 }  // namespace
+
+bool select_regular(const SelSeg* segs_h, int n_segs) {
+  if (n_segs < 2) return n_segs == 1;
+  const int64_t stride = segs_h[1].start - segs_h[0].start;
+  for (int i = 1; i < n_segs; ++i)
+    if (segs_h[i].len != segs_h[0].len || segs_h[i].k != segs_h[0].k ||
+        segs_h[i].start - segs_h[i - 1].start != stride || segs_h[i].out != int64_t(i) * segs_h[0].k)
+      return false;
+  return segs_h[0].out == 0;
+}
 
 hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg* segs_d,
                          int n_segs, int max_len, int32_t* keep, hipStream_t s) {
@@ -527,6 +564,14 @@ hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg
   if (n_segs <= SEL_INLINE) {
     for (int i = 0; i < n_segs; ++i) inl.s[i] = segs_h[i];
     inl.n = n_segs;
+  } else if (select_regular(segs_h, n_segs)) {
+    // equal segments at a fixed stride (one per KV head over the same scores, a batch of
+    // equal-length sequences): the kernels compute each descriptor, nothing is uploaded
+    inl.regular = 1;
+    inl.start0 = segs_h[0].start;
+    inl.stride = segs_h[1].start - segs_h[0].start;
+    inl.len = segs_h[0].len;
+    inl.k = segs_h[0].k;
   }
   // The register path pays a fixed cost per segment (its passes and scans are a chain of
   // block-wide barriers) that the re-reading kernel does not; it wins once a segment is

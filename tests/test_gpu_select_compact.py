@@ -151,6 +151,66 @@ def test_select_many_segments(long_seg):
         off += k
 
 
+@pytest.mark.parametrize("stride", [0, 9000, 9004])
+def test_select_regular_segments_without_a_table(stride):
+    """More than 16 segments of equal length and budget at a fixed stride (0: one per KV
+    head over the same scores; the length: a batch of equal sequences; a gap between
+    them): the kernels compute every descriptor and nothing is uploaded."""
+    r = np.random.default_rng(stride + 5)
+    n, n_segs, k = 9000, 40, 2250
+    s = r.exponential(3.0, (n_segs - 1) * stride + n + 8).astype(np.float32)
+    s[r.integers(0, len(s), 50)] = np.inf
+    starts = [i * stride for i in range(n_segs)]
+    print(f"[select] regular stride={stride}", flush=True)
+    got = _gpu_select(s, starts, [n] * n_segs, [k] * n_segs)
+    for i, st in enumerate(starts):
+        np.testing.assert_array_equal(got[i * k:(i + 1) * k], O.select_keep(s[st:st + n], k),
+                                      err_msg=f"segment {i}")
+
+
+def test_select_many_long_segments_mixed_branches():
+    """More long segments than the GPU has CUs, mixing the distributions and branches of the
+    register path (surprisal-like, +inf filling or not the budget, a narrow band inside a
+    wide range, ulp-spaced, all equal), k = 0 and k = len, zero-length segments and
+    lengths below 8193; budgets over 8192 kept indices leave in several staging windows."""
+    r = np.random.default_rng(2024)
+    n_segs = 700
+    lens = [int(x) for x in r.choice([12288, 32768, 9000 * 4 // 4, 16384, 4096], n_segs)]
+    lens[5] = 0
+    lens = [n - n % 4 for n in lens]
+    segs, ks = [], []
+    for i, n in enumerate(lens):
+        kind = i % 6
+        if kind == 0:
+            x = r.exponential(3.0, n)
+        elif kind == 1:
+            x = r.exponential(3.0, n)
+            x[r.permutation(n)[: n // 2]] = np.inf
+        elif kind == 2:
+            x = 11.0 + r.uniform(0.0, 1e-4, n)
+            m = n // 12
+            x[r.permutation(n)[:m]] = r.uniform(0.0, 100.0, m)
+        elif kind == 3:
+            x = 1.0 + r.integers(0, 200, n) * 2.0 ** -23
+        elif kind == 4:
+            x = np.full(n, np.log(128256.0))
+            x[::97] = np.inf
+        else:
+            x = np.round(r.standard_normal(n), 2)
+            x[::13] = -np.inf
+        segs.append(np.asarray(x, dtype=np.float32))
+        ks.append(int(r.choice([0, 1, max(1, n // 4), n // 2, max(0, n - 1), n])) if n else 0)
+    s = np.concatenate(segs).astype(np.float32)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    print(f"[select] mixed: {n_segs} segments, {len(s)} scores", flush=True)
+    got = _gpu_select(s, starts, lens, ks)
+    off = 0
+    for st, n, k in zip(starts, lens, ks):
+        np.testing.assert_array_equal(got[off:off + k], O.select_keep(s[st:st + n], k),
+                                      err_msg=f"len={n} k={k}")
+        off += k
+
+
 def test_select_overlapping_segments_identical_lists():
     r = np.random.default_rng(9)
     s = r.standard_normal(4096).astype(np.float32)
