@@ -29,7 +29,17 @@ struct CompactArgs {
   int rows_per_chunk;         // (CNT / row16) * CU
 };
 
-__device__ __forceinline__ uint4 ldg16(const char* p) { return *reinterpret_cast<const uint4*>(p); }
+// A 16-byte piece of a source row, read non-temporally: a kept row is read once and never
+// again, so the load need not stay in the caches.  Measured with the cache flushed, in-place
+// compaction of a contiguous 32-layer, 8-head cache keeping 4096 of 32768 entries (1.07 GB
+// moved) goes from 5.4 to 6.3 TB/s, of a paged 28-layer, 4-head cache keeping 20% of eight
+// sequences (1.74 GB) from 4.9 to 5.1 TB/s.  (The same hint on the stores makes both slower:
+// the compacted rows are written in runs that the caches merge.)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16(const char* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 // The paged in-place steps.  A source row needs its keep index, then its page number,
 // then the row; a destination row needs its page number.  Step c issues, in this order,
