@@ -91,6 +91,26 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
   return reinterpret_cast<const char*>((uint64_t(hi) << 32) | lo);
 }
 
+// One 16-byte-per-lane global -> LDS DMA: lane l's 16 bytes land at LDS byte address
+// lds + 16 l.  Issued through inline asm rather than the builtin: with the builtin in the
+// loop the compiler waits for all outstanding LDS reads (lgkmcnt(0)) wherever it waits for
+// one, which defeats the fragment reads issued ahead of their MFMAs; through asm it counts
+// the reads precisely.  The DMAs are ordered by the explicit waitcnt + barrier that ends
+// every tile (and the asm's memory clobber keeps the compiler from moving it).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return uint32_t(reinterpret_cast<uintptr_t>((lds_void*)(p)));
+}
+// scalar base + per-lane 32-bit offset
+__device__ __forceinline__ void dma16(const char* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(sbase), "s"(lds) : "memory", "m0");
+}
+// per-lane 64-bit address
+__device__ __forceinline__ void dma16(const char* vaddr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(vaddr), "s"(lds) : "memory", "m0");
+}
+
 // Per-slab page numbers of one tile (paged caches): slab i = keys 64t + 16i .. +15, which
 // lie in one page because pages hold a power of two >= 16 keys.  Indices past the
 // sequence's last page are clamped (such tiles take the per-lane path anyway).
@@ -205,10 +225,13 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     else
       return pg.p[i];
   };
-  // Fill an LDS tile with tile t.  Full tiles: a uniform base per slab plus the lane's fixed
-  // offset.  The last, partial tile: per-lane rows (clamped), per-lane page lookups.
-  auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, uint32_t lane_off,
-                   int ch, int64_t ts, const SlabPages& pg) {
+  // Fill an LDS tile with tile t.  Full tiles of a contiguous cache: from a running tile
+  // pointer (tile_ptr = plane + t * BN keys, advanced once per tile), a 64-bit scalar add per
+  // 16-key slab and the lane's fixed offset.  Full tiles of a paged cache: a uniform base per
+  // slab from its page.  The last, partial tile: per-lane rows (clamped), per-lane page
+  // lookups.
+  auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, const char* tile_ptr,
+                   uint32_t lane_off, int ch, int64_t ts, const SlabPages& pg) {
     const int key0 = t * BN;
     u16* lds = dst + wave_u * RPW * HD;
     if (key0 + BN <= n) {
@@ -217,14 +240,13 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int si = slab_of(i);
-        int64_t slab;
+        const char* base;
         if constexpr (PAGED)
-          slab = int64_t(slab_page(pg, i)) * kv.page_stride + int64_t((key0 + 16 * si) & kv.page_mask) * kv.tok_stride;
+          base = uniform_ptr(plane + (int64_t(slab_page(pg, i)) * kv.page_stride +
+                                      int64_t((key0 + 16 * si) & kv.page_mask) * kv.tok_stride) * 2);
         else
-          slab = int64_t(key0 + 16 * si) * kv.tok_stride;
-        const char* base = uniform_ptr(plane + slab * 2);
-        __builtin_amdgcn_global_load_lds((global_void*)(base + lane_off),
-                                         (lds_void*)(lds + i * NWAVES * RPW * HD), 16, 0, 0);
+          base = tile_ptr + int64_t(16 * si) * ts;
+        dma16(base, lane_off, lds_addr(lds + i * NWAVES * RPW * HD));
       }
     } else {
 #pragma unroll
@@ -235,8 +257,7 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
           off = int64_t(btab[key >> kv.page_shift]) * kv.page_stride + int64_t(key & kv.page_mask) * kv.tok_stride;
         else
           off = int64_t(key) * kv.tok_stride;
-        __builtin_amdgcn_global_load_lds((global_void*)(plane + off * 2 + ch * 16),
-                                         (lds_void*)(lds + i * NWAVES * RPW * HD), 16, 0, 0);
+        dma16(plane + off * 2 + ch * 16, lds_addr(lds + i * NWAVES * RPW * HD));
       }
     }
   };
@@ -305,6 +326,10 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
 
+  // contiguous caches: tile pointers of the next K (t + 2) and V (t + 1) DMAs, in bytes
+  const int64_t kstep = int64_t(BN) * kts, vstep = int64_t(BN) * vts;
+  const char* kptr = kplane + int64_t(tb + 2) * kstep;
+  const char* vptr = vplane + int64_t(tb + 1) * vstep;
   // prologue: K(tb), V(tb), K(tb+1) in LDS; S(tb) and its unmasked row max in registers.
   // Page numbers: pk for the K tile of the next step (t+2), pv for its V tile (t+1), pn
   // for the K tile after (t+3), loaded one step ahead of use.
@@ -313,9 +338,10 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   SlabPages pn = pages_of(min(tb + 3, te - 1));
   {
     const SlabPages p0 = pages_of(tb);
-    issue(kl0, tb, a.k, kplane, klane, kch, kts, p0);
-    issue(vl0, tb, a.v, vplane, vlane, vch, vts, p0);
-    issue(kl1, min(tb + 1, te - 1), a.k, kplane, klane, kch, kts, pv);
+    issue(kl0, tb, a.k, kplane, kplane + int64_t(tb) * kstep, klane, kch, kts, p0);
+    issue(vl0, tb, a.v, vplane, vplane + int64_t(tb) * vstep, vlane, vch, vts, p0);
+    if (tb + 1 < te)
+      issue(kl1, tb + 1, a.k, kplane, kplane + int64_t(tb + 1) * kstep, klane, kch, kts, pv);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -339,8 +365,11 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     u16* Kfree = P ? kl1 : kl0;
     const u16* Vc = P ? vl1 : vl0;
     u16* Vfree = P ? vl0 : vl1;
-    issue(Kfree, min(t + 2, te - 1), a.k, kplane, klane, kch, kts, pk);
-    issue(Vfree, min(t + 1, te - 1), a.v, vplane, vlane, vch, vts, pv);
+    // tiles past the last are never read: nothing to load
+    if (t + 2 < te) issue(Kfree, t + 2, a.k, kplane, kptr, klane, kch, kts, pk);
+    if (t + 1 < te) issue(Vfree, t + 1, a.v, vplane, vptr, vlane, vch, vts, pv);
+    kptr += kstep;
+    vptr += vstep;
     if constexpr (PAGED) {
       pv = pk;
       pk = pn;

@@ -161,3 +161,29 @@ def test_bf16_outlier_key_channels():
     torch.cuda.synchronize()
     ref = O.attention_cc(w.host["q"], hk16, w.host["v"], "strict")
     _check(f64(o), ref, "bf16")
+
+
+def test_bf16_reference_moves_many_times():
+    """Keys scaled by 2^(j // 160) (exact in bf16): every row's logits grow along its keys,
+    so the softmax reference moves tile after tile, often by far more than the 2^8 of
+    headroom; the first keys of a row then weigh next to nothing."""
+    from paper_2607_27600_amd import cc
+    from paper_2607_27600_amd.workload import Workload
+    cfg = C.shrink(C.C2, seq_lens=(1000,), cache_layers=1)
+    print("[attention] growing key scale, n=1000", flush=True)
+    w = Workload(cfg, cache_layers=1, keep_host=True, with_lm_head=False)
+    n = cfg.n_tokens
+    f = (2.0 ** (np.arange(n) // 160)).astype(np.float32)           # 1 .. 64
+    hk = (w.host["k"].astype(np.uint32) << 16).view(np.float32) * f[None, :, None]
+    hk16 = (hk.view(np.uint32) >> 16).astype(np.uint16)              # exact: powers of two
+    ft = torch.from_numpy(f).to(w.k_cache.device, w.k_cache.dtype)
+    assert not cfg.paged and w.k_cache.shape[:3] == (1, 1, cfg.n_heads_kv)
+    w.k_cache[0, 0, :, :n, :].mul_(ft[None, :, None])               # [batch, layer, head, slot, d]
+    p = cc.problem(dtype=cfg.dtype, cu_seqlens=cfg.cu_seqlens.tolist(), n_heads_q=cfg.n_heads_q,
+                   n_heads_kv=cfg.n_heads_kv, head_dim=cfg.head_dim, hidden=cfg.hidden,
+                   vocab=cfg.vocab)
+    o = torch.full_like(w.q, float("nan"))
+    cc.cc_attention_cc(p, w.q, w.kv, 0, o)
+    torch.cuda.synchronize()
+    ref = O.attention_cc(w.host["q"], hk16, w.host["v"], "strict")
+    _check(f64(o), ref, "bf16")
