@@ -9,6 +9,11 @@ counters named in util():
 
     python -m paper_2607_27600_amd.pmc_summary util <dir>
 
+A fourth merges several counter passes of the same command (dispatch ids line up) into
+issue statistics per kernel: see issue().
+
+    python -m paper_2607_27600_amd.pmc_summary issue <dir1> <dir2> ...
+
 FETCH_SIZE / WRITE_SIZE are in KiB per dispatch.  The driver also copies 1 GiB device to
 device; each counter is scaled by (1 GiB / what it reads for that copy), so the figures are
 calibrated against a transfer of known size.  The record carries the sha256 of gemm.hip;
@@ -118,8 +123,47 @@ def util(run_dir: str, n_xcc: int = 8, n_simd: int = 1024, n_cu: int = 256) -> N
               f"| {100 * busy / (cyc * n_simd):.1f}% | {valu:.2f} | {100 * lds:.1f}% |")
 
 
+def issue(run_dirs: list, n_xcc: int = 8, n_simd: int = 1024, match: str = "") -> None:
+    """Per kernel, from passes holding (between them) SQ_WAVE_CYCLES, SQ_WAIT_ANY,
+    SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_VALU, SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_VALU_MFMA_COEXEC_CYCLES, SQ_INSTS_{MFMA,VALU,SALU,LDS} and GRBM_GUI_ACTIVE.
+
+    SQ_WAVE_CYCLES, SQ_WAIT_ANY and SQ_WAIT_INST_ANY count quad-cycles, so their ratios are
+    fractions of the waves' resident time.  MFMA busy is per SIMD-cycle of the kernel;
+    co-issue is the share of matrix-busy cycles in which another VALU instruction issued.
+    Instruction counts are per MFMA instruction (SQ_INSTS_VALU includes the MFMAs).
+    """
+    merged = {}
+    for d in run_dirs:
+        for k, name, c in _all_counters(os.path.join(d, "run_counter_collection.csv")):
+            m = merged.setdefault(k, [name, {}])
+            for key, v in c.items():
+                if key == "GRBM_GUI_ACTIVE" and key in m[1]:
+                    continue
+                m[1][key] = v
+    print("| dispatch | kernel | cycles | MFMA busy | co-issue | waiting on anything | waiting to issue "
+          "| VALU / MFMA | SALU / MFMA | LDS / MFMA |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
+    for k in sorted(merged):
+        name, c = merged[k]
+        mf = c.get("SQ_INSTS_MFMA", 0.0)
+        if mf == 0.0 or (match and match not in name):
+            continue
+        cyc = c["GRBM_GUI_ACTIVE"] / n_xcc
+        wc = max(c.get("SQ_WAVE_CYCLES", 1.0), 1.0)
+        busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        short = name.replace("cc::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        print(f"| {k} | `{short}` | {cyc:.4g} | {100 * busy / (cyc * n_simd):.1f}% "
+              f"| {100 * c.get('SQ_VALU_MFMA_COEXEC_CYCLES', 0.0) / max(busy, 1.0):.0f}% "
+              f"| {100 * c.get('SQ_WAIT_ANY', 0.0) / wc:.0f}% | {100 * c.get('SQ_WAIT_INST_ANY', 0.0) / wc:.0f}% "
+              f"| {(c.get('SQ_INSTS_VALU', 0.0) - mf) / mf:.2f} | {c.get('SQ_INSTS_SALU', 0.0) / mf:.2f} "
+              f"| {c.get('SQ_INSTS_LDS', 0.0) / mf:.2f} |")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "util":
         util(sys.argv[2])
+    elif sys.argv[1] == "issue":
+        issue(sys.argv[2:])
     else:
         main(*sys.argv[1:5])
