@@ -111,12 +111,23 @@ __device__ __forceinline__ void dma16(const char* vaddr, uint32_t lds) {
                :: "v"(vaddr), "s"(lds) : "memory", "m0");
 }
 
-// Per-slab page numbers of one tile (paged caches): slab i = keys 64t + 16i .. +15, which
-// lie in one page because pages hold a power of two >= 16 keys.  Indices past the
-// sequence's last page are clamped (such tiles take the per-lane path anyway).
-struct SlabPages {
-  int p[4];
-};
+// Page numbers of paged-cache slabs (16 keys, which lie in one page because pages hold a
+// power of two >= 16 keys), fetched with scalar loads at the moment they are needed and
+// waited for at once.  At the start of a step no LDS read is outstanding, so the wait
+// covers only these loads, which hit the scalar cache (16 consecutive table entries per
+// line).  Vector loads of the page numbers would be counted with the tile DMAs, which
+// complete in order: waiting for a page number would wait for every DMA issued before it.
+__device__ __forceinline__ void page_numbers(const int32_t* p0, const int32_t* p1, int& o0, int& o1) {
+  asm volatile("s_load_dword %0, %2, 0x0\n\ts_load_dword %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+               : "=&s"(o0), "=&s"(o1) : "s"(p0), "s"(p1) : "memory");
+}
+__device__ __forceinline__ void page_numbers(const int32_t* p0, const int32_t* p1, const int32_t* p2,
+                                             const int32_t* p3, int& o0, int& o1, int& o2, int& o3) {
+  asm volatile("s_load_dword %0, %4, 0x0\n\ts_load_dword %1, %5, 0x0\n\t"
+               "s_load_dword %2, %6, 0x0\n\ts_load_dword %3, %7, 0x0\n\ts_waitcnt lgkmcnt(0)"
+               : "=&s"(o0), "=&s"(o1), "=&s"(o2), "=&s"(o3)
+               : "s"(p0), "s"(p1), "s"(p2), "s"(p3) : "memory");
+}
 
 template <int HD, bool PAGED>
 __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
@@ -206,24 +217,11 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
                                       : kv_off<false>(a.v, b, a.layer, kvh, 0)) * 2;
   const int32_t* btab = PAGED ? a.k.block_table + int64_t(b) * a.k.max_pages : nullptr;
   const int last_page = PAGED ? (n - 1) >> a.k.page_shift : 0;
-  auto pages_of = [&](int t) {
-    SlabPages s;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      s.p[i] = PAGED ? btab[min((t * BN + 16 * i) >> a.k.page_shift, last_page)] : 0;
-    return s;
-  };
   // The 16-key slab of load instruction i (wave-uniform): at HD = 128 the four waves' rows
   // of one instruction form slab i; at HD = 64 waves 0-1 fill slab 2i and waves 2-3 slab
-  // 2i + 1.  The page of that slab is picked without indexing the array by a variable.
+  // 2i + 1.
   auto slab_of = [&](int i) {
     return RPW * NWAVES > 16 ? (RPW * NWAVES / 16) * i + (RPW * wave_u) / 16 : i;
-  };
-  auto slab_page = [&](const SlabPages& pg, int i) {
-    if constexpr (RPW * NWAVES > 16)
-      return (wave_u >> 1) ? pg.p[2 * i + 1] : pg.p[2 * i];
-    else
-      return pg.p[i];
   };
   // Fill an LDS tile with tile t.  Full tiles of a contiguous cache: from a running tile
   // pointer (tile_ptr = plane + t * BN keys, advanced once per tile), a 64-bit scalar add per
@@ -231,18 +229,28 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   // slab from its page.  The last, partial tile: per-lane rows (clamped), per-lane page
   // lookups.
   auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, const char* tile_ptr,
-                   uint32_t lane_off, int ch, int64_t ts, const SlabPages& pg) {
+                   uint32_t lane_off, int ch, int64_t ts) {
     const int key0 = t * BN;
     u16* lds = dst + wave_u * RPW * HD;
     if (key0 + BN <= n) {
       // keep the 32-bit offset opaque here so that it is not widened outside the loop
       asm volatile("" : "+v"(lane_off));
+      int pg[NI];
+      if constexpr (PAGED) {
+        const int32_t* pp[NI];
+#pragma unroll
+        for (int i = 0; i < NI; ++i) pp[i] = btab + min((key0 + 16 * slab_of(i)) >> kv.page_shift, last_page);
+        if constexpr (NI == 4)
+          page_numbers(pp[0], pp[1], pp[2], pp[3], pg[0], pg[1], pg[2], pg[3]);
+        else
+          page_numbers(pp[0], pp[1], pg[0], pg[1]);
+      }
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int si = slab_of(i);
         const char* base;
         if constexpr (PAGED)
-          base = uniform_ptr(plane + (int64_t(slab_page(pg, i)) * kv.page_stride +
+          base = uniform_ptr(plane + (int64_t(pg[i]) * kv.page_stride +
                                       int64_t((key0 + 16 * si) & kv.page_mask) * kv.tok_stride) * 2);
         else
           base = tile_ptr + int64_t(16 * si) * ts;
@@ -331,18 +339,9 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const char* kptr = kplane + int64_t(tb + 2) * kstep;
   const char* vptr = vplane + int64_t(tb + 1) * vstep;
   // prologue: K(tb), V(tb), K(tb+1) in LDS; S(tb) and its unmasked row max in registers.
-  // Page numbers: pk for the K tile of the next step (t+2), pv for its V tile (t+1), pn
-  // for the K tile after (t+3), loaded one step ahead of use.
-  SlabPages pk = pages_of(min(tb + 2, te - 1));
-  SlabPages pv = pages_of(min(tb + 1, te - 1));
-  SlabPages pn = pages_of(min(tb + 3, te - 1));
-  {
-    const SlabPages p0 = pages_of(tb);
-    issue(kl0, tb, a.k, kplane, kplane + int64_t(tb) * kstep, klane, kch, kts, p0);
-    issue(vl0, tb, a.v, vplane, vplane + int64_t(tb) * vstep, vlane, vch, vts, p0);
-    if (tb + 1 < te)
-      issue(kl1, tb + 1, a.k, kplane, kplane + int64_t(tb + 1) * kstep, klane, kch, kts, pv);
-  }
+  issue(kl0, tb, a.k, kplane, kplane + int64_t(tb) * kstep, klane, kch, kts);
+  issue(vl0, tb, a.v, vplane, vplane + int64_t(tb) * vstep, vlane, vch, vts);
+  if (tb + 1 < te) issue(kl1, tb + 1, a.k, kplane, kplane + int64_t(tb + 1) * kstep, klane, kch, kts);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   f32x16 sa[2], sb[2];
@@ -366,15 +365,10 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     const u16* Vc = P ? vl1 : vl0;
     u16* Vfree = P ? vl0 : vl1;
     // tiles past the last are never read: nothing to load
-    if (t + 2 < te) issue(Kfree, t + 2, a.k, kplane, kptr, klane, kch, kts, pk);
-    if (t + 1 < te) issue(Vfree, t + 1, a.v, vplane, vptr, vlane, vch, vts, pv);
+    if (t + 2 < te) issue(Kfree, t + 2, a.k, kplane, kptr, klane, kch, kts);
+    if (t + 1 < te) issue(Vfree, t + 1, a.v, vplane, vptr, vlane, vch, vts);
     kptr += kstep;
     vptr += vstep;
-    if constexpr (PAGED) {
-      pv = pk;
-      pk = pn;
-      pn = pages_of(min(t + 4, te - 1));
-    }
     bf16x8 kf[4];
     kf[0] = kfrag(Kn, 0);
     kf[1] = kfrag(Kn, 1);
