@@ -27,6 +27,34 @@ __device__ __forceinline__ SelSeg seg_desc(const SelInline& inl, const SelSeg* s
   return b < inl.n ? inl.s[b] : segs[b];
 }
 
+// Wave-wide inclusive scans and reductions on DPP lane moves (VALU only, no LDS round
+// trip): shifts of 1, 2, 4 and 8 lanes inside each row of 16 (lanes without a source keep
+// the identity), then the last lane of row 0 (2) added into row 1 (3), then lane 31 into
+// rows 2 and 3.  Lane i ends with op over lanes 0..i.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t x, uint32_t identity) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(identity), int(x), CTRL, ROWS, 0xf, false));
+}
+template <class Op>
+__device__ __forceinline__ uint32_t wave_scan(uint32_t x, uint32_t identity, Op op) {
+  x = op(x, dpp_move<0x111, 0xf>(x, identity));   // row_shr:1
+  x = op(x, dpp_move<0x112, 0xf>(x, identity));   // row_shr:2
+  x = op(x, dpp_move<0x114, 0xf>(x, identity));   // row_shr:4
+  x = op(x, dpp_move<0x118, 0xf>(x, identity));   // row_shr:8
+  x = op(x, dpp_move<0x142, 0xa>(x, identity));   // row_bcast:15 into rows 1 and 3
+  x = op(x, dpp_move<0x143, 0xc>(x, identity));   // row_bcast:31 into rows 2 and 3
+  return x;
+}
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
+  (void)lane;
+  return wave_scan(x, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+}
+// the reduction over the whole wave, in every lane
+template <class Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, uint32_t identity, Op op) {
+  return uint32_t(__builtin_amdgcn_readlane(int(wave_scan(x, identity, op)), 63));
+}
+
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;   // NaN: lowest
@@ -91,12 +119,7 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
         c[j] = hist[255 - 4 * lane - j];
         sum += c[j];
       }
-      uint32_t incl = sum;   // inclusive scan over lanes (descending digit order)
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t t = __shfl_up(incl, off);
-        if (lane >= off) incl += t;
-      }
+      const uint32_t incl = wave_incl_scan(sum, lane);   // over lanes (descending digits)
       const uint32_t excl = incl - sum;
       if (excl < rem && incl >= rem) {
         uint32_t acc = excl;
@@ -182,15 +205,6 @@ struct Pick {
   uint32_t digit, rem, cnt;
 };
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t t = uint32_t(__shfl_up(int(x), off));
-    if (lane >= off) x += t;
-  }
-  return x;
-}
-
 // Run by one whole wave: in a histogram of 64 * BPL bins searched from the highest bin down,
 // the bin holding the rem-th largest counted key (1 <= rem <= total), the rank left inside
 // it and its count; every lane receives the result.  Level 1: lane l sums bins
@@ -215,14 +229,14 @@ __device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int
   const uint32_t incl = wave_incl_scan(sum, lane);
   const uint64_t over = __ballot(incl >= rem);
   const int owner = over ? int(__builtin_ctzll(over)) : 63;   // rem <= total: some lane does
-  const uint32_t before = uint32_t(__shfl(int(incl - sum), owner));
+  const uint32_t before = uint32_t(__builtin_amdgcn_readlane(int(incl - sum), owner));
   const int top = NB - BPL * owner - 1;              // the owner's highest bin
   const uint32_t c = lane < BPL ? h[top - lane] : 0u;
   const uint32_t incl2 = wave_incl_scan(c, lane);
   const uint64_t hit = __ballot(lane < BPL && before + incl2 >= rem);
   const int j = hit ? int(__builtin_ctzll(hit)) : BPL - 1;
-  const uint32_t cj = uint32_t(__shfl(int(c), j));
-  const uint32_t ij = uint32_t(__shfl(int(incl2), j));
+  const uint32_t cj = uint32_t(__builtin_amdgcn_readlane(int(c), j));
+  const uint32_t ij = uint32_t(__builtin_amdgcn_readlane(int(incl2), j));
   return {uint32_t(top - j), rem - before - (ij - cj), cj};
 }
 
@@ -241,12 +255,7 @@ __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
   }
   // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1)
-#pragma unroll
-    for (int q = 0; q < RCH / 2; ++q) {
-      const uint32_t t = uint32_t(__shfl_up(int(inc[q]), off));
-      if (lane >= off) inc[q] += t;
-    }
+  for (int q = 0; q < RCH / 2; ++q) inc[q] = wave_incl_scan(inc[q], lane);
   if (lane == 63) *reinterpret_cast<uint4*>(wtot[wave]) = make_uint4(inc[0], inc[1], inc[2], inc[3]);
   __syncthreads();
   uint32_t all[RCH / 2] = {0u, 0u, 0u, 0u}, bef[RCH / 2] = {0u, 0u, 0u, 0u};
@@ -344,12 +353,9 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
     kmaxf = v && !inf ? max(kmaxf, key[j]) : kmaxf;
     ninf += uint32_t(v && inf);
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    kmin = min(kmin, uint32_t(__shfl_xor(int(kmin), off)));
-    kmaxf = max(kmaxf, uint32_t(__shfl_xor(int(kmaxf), off)));
-    ninf += uint32_t(__shfl_xor(int(ninf), off));
-  }
+  kmin = wave_reduce(kmin, 0xffffffffu, [](uint32_t a, uint32_t b) { return min(a, b); });
+  kmaxf = wave_reduce(kmaxf, 0u, [](uint32_t a, uint32_t b) { return max(a, b); });
+  ninf = wave_reduce(ninf, 0u, [](uint32_t a, uint32_t b) { return a + b; });
   if (lane == 0) {
     L.red[0][wave] = kmin;
     L.red[1][wave] = kmaxf;
@@ -437,7 +443,7 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
           const uint32_t incl = wave_incl_scan(mine, lane);
           uint32_t base = 0u;
           if (lane == 63) base = atomicAdd(&L.sh_ncand, incl);
-          uint32_t pos = uint32_t(__shfl(int(base), 63)) + incl - mine;
+          uint32_t pos = uint32_t(__builtin_amdgcn_readlane(int(base), 63)) + incl - mine;
 #pragma unroll
           for (int j = 0; j < RPT; ++j) {
             if ((cmask >> j) & 1u) {
