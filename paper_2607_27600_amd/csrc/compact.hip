@@ -26,6 +26,7 @@ struct CompactArgs {
   const CompactList* lists;
   const CompactPlane* planes;
   int n_planes;
+  int n_tensors;              // 1 (ids layout of one tensor) or 2 (keys and values)
   int rows_per_chunk;         // (CNT / row16) * CU
 };
 
@@ -122,8 +123,10 @@ __device__ __forceinline__ void compact_paged_steps(const CompactArgs& a, const 
 
 template <bool PAGED>
 __global__ __launch_bounds__(CNT) void compact_in_place_kernel(CompactArgs a) {
-  const int tensor = blockIdx.x / a.n_planes;
-  const CompactPlane P = a.planes[blockIdx.x % a.n_planes];
+  // plane-major: the keys and the values of a plane are adjacent workgroups, so the planes
+  // (sorted longest first) start in that order for both tensors when not all are resident
+  const int tensor = blockIdx.x % a.n_tensors;
+  const CompactPlane P = a.planes[blockIdx.x / a.n_tensors];
   const CompactList L = a.lists[P.list];
   const int32_t* keep = a.keep + L.keep_off;
   const int k = L.k;
@@ -189,8 +192,8 @@ __global__ __launch_bounds__(CNT) void compact_in_place_kernel(CompactArgs a) {
 
 template <bool PAGED>
 __global__ __launch_bounds__(CNT) void compact_kernel(CompactArgs a) {
-  const int tensor = blockIdx.x / a.n_planes;
-  const CompactPlane P = a.planes[blockIdx.x % a.n_planes];
+  const int tensor = blockIdx.x % a.n_tensors;
+  const CompactPlane P = a.planes[blockIdx.x / a.n_tensors];
   const CompactList L = a.lists[P.list];
   const int32_t* keep = a.keep + L.keep_off;
   const int k = L.k;
@@ -265,6 +268,7 @@ hipError_t launch_compact(const CompactLaunch& c, hipStream_t s) {
   a.lists = c.lists_d;
   a.planes = c.planes_d;
   a.n_planes = c.n_planes;
+  a.n_tensors = c.n_tensors;
   a.rows_per_chunk = (CNT / a.row16) * CU;
   if (c.n_planes > 0) {
     if (c.in_place) {
