@@ -17,7 +17,7 @@ namespace cc {
 namespace {
 
 constexpr int CNT = 256;      // threads per workgroup
-constexpr int CU = 8;         // 16-byte rows pieces in flight per thread per chunk
+constexpr int CU = 5;         // 16-byte row pieces in flight per thread per chunk
 
 struct CompactArgs {
   KvView src[2], dst[2];
