@@ -184,8 +184,8 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
 //  - Emission: a thread's flagged keys per chunk are counted, and one batched scan over
 //    the workgroup (8 chunk counts per thread, two per word) gives every flagged key its
 //    rank in index order: first for the ties (when not all of them are kept), then for
-//    the kept keys, which are staged in LDS at their ranks (8192 at a time) and written
-//    out as consecutive words.
+//    the kept keys, which each thread stores at their ranks (consecutive keys of a chunk
+//    at consecutive ranks; staging them through LDS to store whole runs measured slower).
 constexpr int RNT = 1024;
 constexpr int RWAVES = RNT / 64;
 constexpr int RCW = 4;                 // scores per thread per chunk
@@ -199,7 +199,6 @@ constexpr int SD = 11;                 // bits of a block-wide digit
 constexpr int SBINS = 1 << SD;
 constexpr int WD = 9;                  // bits of a digit of the one-wave finish
 constexpr int WBINS = 1 << WD;
-constexpr int OWIN = 8192;             // kept indices staged in LDS per window
 
 struct Pick {
   uint32_t digit, rem, cnt;
@@ -284,7 +283,6 @@ struct RegLds {
   uint32_t hist[SBINS];
   uint32_t cand[CMAX];
   uint32_t whist[WBINS];
-  int32_t stg[OWIN];
   uint32_t red[3][RWAVES];
   __attribute__((aligned(16))) uint32_t wtot[2][RWAVES][RCH / 2];
   uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
@@ -346,12 +344,23 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
 
   // extremes of the segment and its number of +inf keys; the histogram is cleared meanwhile
   uint32_t kmin = 0xffffffffu, kmaxf = 0u, ninf = 0u;
+  if (vbits == 0xffffffffu) {
+    // every key of this thread lies inside the segment
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    const bool v = valid(j), inf = key[j] == KINF;
-    kmin = v ? min(kmin, key[j]) : kmin;
-    kmaxf = v && !inf ? max(kmaxf, key[j]) : kmaxf;
-    ninf += uint32_t(v && inf);
+    for (int j = 0; j < RPT; ++j) {
+      const bool inf = key[j] == KINF;
+      kmin = min(kmin, key[j]);
+      kmaxf = max(kmaxf, inf ? 0u : key[j]);
+      ninf += uint32_t(inf);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const bool v = valid(j), inf = key[j] == KINF;
+      kmin = v ? min(kmin, key[j]) : kmin;
+      kmaxf = v && !inf ? max(kmaxf, key[j]) : kmaxf;
+      ninf += uint32_t(v && inf);
+    }
   }
   kmin = wave_reduce(kmin, 0xffffffffu, [](uint32_t a, uint32_t b) { return min(a, b); });
   kmaxf = wave_reduce(kmaxf, 0u, [](uint32_t a, uint32_t b) { return max(a, b); });
@@ -529,25 +538,17 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
   chunk_offsets(take, base, L.wtot[1], lane, wave);
   int t4s = 4 * tid;
   asm volatile("" : "+v"(t4s));
-  // A thread's kept keys of chunk c take consecutive ranks base[c], base[c] + 1, ...: each
-  // is staged at its rank in LDS, OWIN ranks at a time, and the window leaves as
-  // consecutive words (one coalesced store per thread and 1024 indices).
-  for (int w0 = 0; w0 < k; w0 += OWIN) {
+  // kept keys of chunk c at ranks base[c], base[c] + 1, ...: stored directly
 #pragma unroll
-    for (int c = 0; c < RCH; ++c) {
-      uint32_t r = base[c] - uint32_t(w0);
+  for (int c = 0; c < RCH; ++c) {
+    uint32_t r = base[c];
 #pragma unroll
-      for (int u = 0; u < RCW; ++u) {
-        if ((take >> (RCW * c + u)) & 1u) {
-          if (r < uint32_t(OWIN)) L.stg[r] = c * RCHUNK + t4s + u;
-          ++r;
-        }
+    for (int u = 0; u < RCW; ++u) {
+      if ((take >> (RCW * c + u)) & 1u) {
+        out[r] = c * RCHUNK + t4s + u;
+        ++r;
       }
     }
-    __syncthreads();
-    const int m = min(OWIN, k - w0);
-    for (int i = tid; i < m; i += RNT) out[w0 + i] = L.stg[i];
-    if (w0 + OWIN < k) __syncthreads();   // the next window reuses the staging area
   }
 }
 
