@@ -167,25 +167,31 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
 // Segments of up to RMAX scores: the workgroup reads its segment once into registers and
 // never touches it again.  The segment is cut into 8 chunks of 4096 scores; thread t of
 // 1024 holds scores 4t .. 4t+3 of every chunk (one 16-byte load per chunk, 1 KB per wave
-// instruction), so index order is (chunk, thread, slot).
-//  - Extremes: kmin over the segment, kmaxf over its keys other than +inf, and the number
-//    of +inf keys.  When the +inf keys fill the budget they hold the threshold.  Otherwise
-//    the radix digits run on rel = key - kmin over the B = bit length of kmaxf - kmin
-//    bits, so the first digit spreads over the finite scores' actual range (the +inf of a
-//    sequence's last entry would otherwise squeeze them all into one bucket).
-//  - One 11-bit pass over every key into a 2048-bin LDS histogram.  An 11-bit digit leaves
-//    about an eighth of the keys an 8-bit one would in the bucket that holds the threshold,
-//    and spreads a wave's atomics over more bins, so fewer lanes of one instruction
-//    collide.  When that bucket has at most CMAX keys, their low bits are copied to LDS and
-//    one wave finishes the lower digits on that list (9 bits a pass, no block-wide
-//    barrier); otherwise further 11-bit block-wide passes run over the registers.
+// instruction), so index order is (chunk, thread, slot).  The kernel is bound by vector ALU
+// issue, so every per-key step is kept to a few instructions:
+//  - Keys: the float's sign and magnitude turned into a signed two's complement integer
+//    (-0 and +0 both become 0).  NaN keys then lie outside the keys of -inf .. +inf; a
+//    segment that holds any (seen in its extremes) sets them all to one key below -inf.
+//  - Extremes: the smallest key kmin and the largest key other than +inf (a max over
+//    key + 2^23, where +inf alone wraps to the bottom).  The radix digits run on
+//    rel = min(key - kmin, rcap), rcap = that largest key - kmin + 1: +inf keys become rcap,
+//    one above every finite key, and the first digit spreads over the finite scores'
+//    actual range (the +inf of a sequence's last entry would otherwise squeeze them all
+//    into one bucket).
+//  - One 11-bit pass over every key (no test: the first digit holds the top bits of every
+//    rel) into a 2048-bin LDS histogram.  An 11-bit digit leaves about an eighth of the keys
+//    an 8-bit one would in the bucket that holds the threshold, and spreads a wave's atomics
+//    over more bins, so fewer lanes of one instruction collide.  When that bucket has at
+//    most CMAX keys, waves that hold any of them copy their low bits to LDS and one wave
+//    finishes the lower digits on that list (9 bits a pass, no block-wide barrier);
+//    otherwise further 11-bit block-wide passes run over the registers.
 //  - Bucket searches are two-level wave scans: lane sums over the lanes' bin ranges, then
 //    the bins of the lane that holds the rank.
 //  - Emission: a thread's flagged keys per chunk are counted, and one batched scan over
 //    the workgroup (8 chunk counts per thread, two per word) gives every flagged key its
 //    rank in index order: first for the ties (when not all of them are kept), then for
 //    the kept keys, which each thread stores at their ranks (consecutive keys of a chunk
-//    at consecutive ranks; staging them through LDS to store whole runs measured slower).
+//    at consecutive ranks) through a buffer descriptor bounded by the segment's budget.
 constexpr int RNT = 1024;
 constexpr int RWAVES = RNT / 64;
 constexpr int RCW = 4;                 // scores per thread per chunk
@@ -194,11 +200,42 @@ constexpr int RCHUNK = RNT * RCW;      // scores per chunk
 constexpr int RPT = RCH * RCW;         // scores per thread
 constexpr int RMAX = RNT * RPT;
 constexpr int CMAX = 4096;             // candidate list of the one-wave finish
-constexpr uint32_t KINF = 0xff800000u;   // order_key(+inf): the largest key
 constexpr int SD = 11;                 // bits of a block-wide digit
 constexpr int SBINS = 1 << SD;
 constexpr int WD = 9;                  // bits of a digit of the one-wave finish
 constexpr int WBINS = 1 << WD;
+constexpr int32_t KEY_PINF = 0x7f800000;    // key of +inf
+constexpr int32_t KEY_NINF = -0x7f800000;   // key of -inf
+constexpr int32_t KEY_NAN = KEY_NINF - 1;   // key of every NaN
+constexpr uint32_t FIN_SHIFT = 0x00800000u; // key + FIN_SHIFT wraps +inf, and only +inf, to INT_MIN
+constexpr int32_t I32_MAX = 0x7fffffff;
+constexpr int32_t I32_MIN = -I32_MAX - 1;
+
+// Signed order key of a float's bits: sign and magnitude to two's complement.
+__device__ __forceinline__ int32_t skey(uint32_t u) {
+  const uint32_t t = uint32_t(int32_t(u) >> 31);
+  return int32_t((u ^ t) + (t & 0x80000001u));
+}
+
+// Inclusive scan inside each row of 16 lanes (row 0 holds lanes 0..15).
+__device__ __forceinline__ uint32_t row_scan(uint32_t x) {
+  x += dpp_move<0x111, 0xf>(x, 0u);
+  x += dpp_move<0x112, 0xf>(x, 0u);
+  x += dpp_move<0x114, 0xf>(x, 0u);
+  x += dpp_move<0x118, 0xf>(x, 0u);
+  return x;
+}
+// op over lanes 0..15, in every lane
+template <class Op>
+__device__ __forceinline__ uint32_t row0_reduce(uint32_t x, uint32_t identity, Op op) {
+  x = op(x, dpp_move<0x111, 0xf>(x, identity));
+  x = op(x, dpp_move<0x112, 0xf>(x, identity));
+  x = op(x, dpp_move<0x114, 0xf>(x, identity));
+  x = op(x, dpp_move<0x118, 0xf>(x, identity));
+  return uint32_t(__builtin_amdgcn_readlane(int(x), 15));
+}
+constexpr auto imin = [](uint32_t a, uint32_t b) { return uint32_t(min(int32_t(a), int32_t(b))); };
+constexpr auto imax = [](uint32_t a, uint32_t b) { return uint32_t(max(int32_t(a), int32_t(b))); };
 
 struct Pick {
   uint32_t digit, rem, cnt;
@@ -241,8 +278,10 @@ __device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int
 
 // Ranks in index order of the keys flagged in m (bit 4c + i: slot i of chunk c): base[c]
 // = flagged keys before this thread's part of chunk c.  wtot: [RWAVES][RCH / 2] words of
-// LDS owned by this call (16-byte aligned rows).  Contains one barrier.
+// LDS owned by this call (16-byte aligned rows); wave: the wave's index, uniform.  Contains
+// one barrier.  After it, lanes 0..15 of every wave scan the 16 waves' totals.
 static_assert(RPT == 32, "one bit per key in a 32-bit mask");
+static_assert(RWAVES == 16, "the waves' totals are combined in one row of 16 lanes");
 __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
                                               uint32_t (*wtot)[RCH / 2], int lane, int wave) {
   uint32_t own[RCH / 2], inc[RCH / 2];
@@ -250,32 +289,25 @@ __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
   for (int q = 0; q < RCH / 2; ++q) {
     own[q] = uint32_t(__popc((m >> (8 * q)) & 0xfu)) |
              (uint32_t(__popc((m >> (8 * q + 4)) & 0xfu)) << 16);
-    inc[q] = own[q];
+    // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
+    inc[q] = wave_incl_scan(own[q], lane);
   }
-  // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
-#pragma unroll
-  for (int q = 0; q < RCH / 2; ++q) inc[q] = wave_incl_scan(inc[q], lane);
   if (lane == 63) *reinterpret_cast<uint4*>(wtot[wave]) = make_uint4(inc[0], inc[1], inc[2], inc[3]);
   __syncthreads();
-  uint32_t all[RCH / 2] = {0u, 0u, 0u, 0u}, bef[RCH / 2] = {0u, 0u, 0u, 0u};
-#pragma unroll
-  for (int w = 0; w < RWAVES; ++w) {
-    const uint4 t = *reinterpret_cast<const uint4*>(wtot[w]);
-    const uint32_t tv[4] = {t.x, t.y, t.z, t.w};
-#pragma unroll
-    for (int q = 0; q < RCH / 2; ++q) {
-      all[q] += tv[q];
-      bef[q] += w < wave ? tv[q] : 0u;
-    }
-  }
+  uint4 t = make_uint4(0u, 0u, 0u, 0u);
+  if (lane < RWAVES) t = *reinterpret_cast<const uint4*>(wtot[lane]);
+  const uint32_t tv[4] = {t.x, t.y, t.z, t.w};
   uint32_t run = 0u;
 #pragma unroll
   for (int q = 0; q < RCH / 2; ++q) {
-    const uint32_t mine = bef[q] + inc[q] - own[q];
+    const uint32_t sc = row_scan(tv[q]);
+    const uint32_t all = uint32_t(__builtin_amdgcn_readlane(int(sc), RWAVES - 1));
+    const uint32_t bef = uint32_t(__builtin_amdgcn_readlane(int(sc - tv[q]), wave));
+    const uint32_t mine = bef + inc[q] - own[q];
     base[2 * q] = run + (mine & 0xffffu);
-    run += all[q] & 0xffffu;
+    run += all & 0xffffu;
     base[2 * q + 1] = run + (mine >> 16);
-    run += all[q] >> 16;
+    run += all >> 16;
   }
 }
 
@@ -283,19 +315,32 @@ struct RegLds {
   uint32_t hist[SBINS];
   uint32_t cand[CMAX];
   uint32_t whist[WBINS];
-  uint32_t red[3][RWAVES];
+  uint32_t red[5][RWAVES];
   __attribute__((aligned(16))) uint32_t wtot[2][RWAVES][RCH / 2];
   uint32_t sh_digit, sh_rem, sh_cnt, sh_ncand;
 };
+
+// The descriptor's fields in scalar registers (a descriptor picked from the kernel
+// arguments by the block index is otherwise not known to be uniform).
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(uint64_t(x)))));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readfirstlane(int(uint32_t(uint64_t(x) >> 32))));
+  return int64_t((uint64_t(hi) << 32) | lo);
+}
 
 __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restrict__ scores,
                                                            const SelSeg* __restrict__ segs,
                                                            SelInline inl,
                                                            int32_t* __restrict__ keep) {
   __shared__ __attribute__((aligned(16))) RegLds L;
-  const SelSeg sg = seg_desc(inl, segs, int(blockIdx.x));
+  SelSeg sg = seg_desc(inl, segs, int(blockIdx.x));
+  sg.start = uniform64(sg.start);
+  sg.out = uniform64(sg.out);
+  sg.len = __builtin_amdgcn_readfirstlane(sg.len);
+  sg.k = __builtin_amdgcn_readfirstlane(sg.k);
   const int n = sg.len, k = sg.k;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int32_t* out = keep + sg.out;
   if (k <= 0) return;
   if (k >= n) {
@@ -327,8 +372,6 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
       key[j] = *reinterpret_cast<const uint32_t*>(sb + off);
     }
   }
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) key[j] = order_key(__uint_as_float(key[j]));
   // Index arithmetic restarts from an opaque copy of 4*tid here and before the stores, so
   // the compiler recomputes it instead of keeping 64 indices (and their compare masks)
   // live across the kernel.  vbits: bit j set when key j lies inside the segment.
@@ -340,194 +383,228 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
     const int nv = min(max(n - c * RCHUNK - t4, 0), RCW);
     vbits |= ((1u << nv) - 1u) << (RCW * c);
   }
+  const bool whole = vbits == 0xffffffffu;   // every key of this thread lies inside the segment
   auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
 
-  // extremes of the segment and its number of +inf keys; the histogram is cleared meanwhile
-  uint32_t kmin = 0xffffffffu, kmaxf = 0u, ninf = 0u;
-  if (vbits == 0xffffffffu) {
-    // every key of this thread lies inside the segment
+  // keys; their smallest, their largest (NaN detection) and the largest + FIN_SHIFT
+  int32_t mn = I32_MAX, mx = I32_MIN, mf = I32_MIN;
+  if (whole) {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
-      const bool inf = key[j] == KINF;
-      kmin = min(kmin, key[j]);
-      kmaxf = max(kmaxf, inf ? 0u : key[j]);
-      ninf += uint32_t(inf);
+      const int32_t s = skey(key[j]);
+      key[j] = uint32_t(s);
+      mn = min(mn, s);
+      mx = max(mx, s);
+      mf = max(mf, int32_t(uint32_t(s) + FIN_SHIFT));
     }
   } else {
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
-      const bool v = valid(j), inf = key[j] == KINF;
-      kmin = v ? min(kmin, key[j]) : kmin;
-      kmaxf = v && !inf ? max(kmaxf, key[j]) : kmaxf;
-      ninf += uint32_t(v && inf);
+      const int32_t s = skey(key[j]);
+      key[j] = uint32_t(s);
+      const bool v = valid(j);
+      mn = v ? min(mn, s) : mn;
+      mx = v ? max(mx, s) : mx;
+      mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
     }
   }
-  kmin = wave_reduce(kmin, 0xffffffffu, [](uint32_t a, uint32_t b) { return min(a, b); });
-  kmaxf = wave_reduce(kmaxf, 0u, [](uint32_t a, uint32_t b) { return max(a, b); });
-  ninf = wave_reduce(ninf, 0u, [](uint32_t a, uint32_t b) { return a + b; });
-  if (lane == 0) {
-    L.red[0][wave] = kmin;
-    L.red[1][wave] = kmaxf;
-    L.red[2][wave] = ninf;
+  {
+    const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
+    const uint32_t r1 = wave_reduce(uint32_t(mx), uint32_t(I32_MIN), imax);
+    const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
+    if (lane == 0) {
+      L.red[0][wave] = r0;
+      L.red[1][wave] = r1;
+      L.red[2][wave] = r2;
+    }
   }
   for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
   if (tid == 0) L.sh_ncand = 0u;
   __syncthreads();
-  kmin = L.red[0][0];
-  kmaxf = L.red[1][0];
-  ninf = L.red[2][0];
+  mn = int32_t(row0_reduce(lane < RWAVES ? L.red[0][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
+  mx = int32_t(row0_reduce(lane < RWAVES ? L.red[1][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
+  mf = int32_t(row0_reduce(lane < RWAVES ? L.red[2][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
+  if (mn < KEY_NINF || mx > KEY_PINF) {
+    // some score is NaN: every NaN key becomes KEY_NAN and the extremes are taken again
+    // (KEY_NAN + FIN_SHIFT stays clear of INT_MIN)
+    mn = I32_MAX;
+    mf = I32_MIN;
 #pragma unroll
-  for (int w = 1; w < RWAVES; ++w) {
-    kmin = min(kmin, L.red[0][w]);
-    kmaxf = max(kmaxf, L.red[1][w]);
-    ninf += L.red[2][w];
+    for (int j = 0; j < RPT; ++j) {
+      int32_t s = int32_t(key[j]);
+      s = (s < KEY_NINF || s > KEY_PINF) ? KEY_NAN : s;
+      key[j] = uint32_t(s);
+      const bool v = valid(j);
+      mn = v ? min(mn, s) : mn;
+      mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
+    }
+    const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
+    const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
+    if (lane == 0) {
+      L.red[3][wave] = r0;
+      L.red[4][wave] = r2;
+    }
+    __syncthreads();
+    mn = int32_t(row0_reduce(lane < RWAVES ? L.red[3][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
+    mf = int32_t(row0_reduce(lane < RWAVES ? L.red[4][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
   }
-  // From here on the registers hold rel = key - kmin: the order is unchanged and +inf
-  // keys are the ones equal to rinf.  Padding (indices past the end) becomes rel 0, the
-  // smallest key: it is last in index order, and since k < n the kept ties (lowest index
-  // first) never reach it, so it changes no selection; counts below may include it.
+  // From here on the registers hold rel = min(key - kmin, rcap): the order is unchanged and
+  // +inf keys (if any) equal rcap.  With no key below +inf, every rel is 0.  Padding
+  // (indices past the end) becomes rel 0, the smallest key: it is last in index order, and
+  // since k < n the kept ties (lowest index first) never reach it, so it changes no
+  // selection; counts below may include it.
+  const uint32_t kmin = uint32_t(mn);
+  const uint32_t rcap = mf != I32_MIN ? uint32_t(mf) - FIN_SHIFT - kmin + 1u : 0u;
+  if (whole) {
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? key[j] - kmin : 0u;
-  const uint32_t rinf = KINF - kmin;
+    for (int j = 0; j < RPT; ++j) key[j] = min(key[j] - kmin, rcap);
+  } else {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? min(key[j] - kmin, rcap) : 0u;
+  }
 
   // T: the k-th largest rel; keep `rem` of the keys equal to T, of which there are `cnt`
   // (a count that may include padding)
-  uint32_t T, rem, cnt;
-  if (ninf >= uint32_t(k)) {
-    T = rinf;
-    rem = uint32_t(k);
-    cnt = ninf;
+  uint32_t rem = uint32_t(k), cnt;
+  uint32_t prefix = 0u;   // rel >> hi of the keys still in the running
+  const int B = rcap ? 32 - __clz(rcap) : 0;   // rel < 2^B
+  if (B == 0) {
+    cnt = uint32_t(n);   // every key is 0
   } else {
-    // at least one key is below +inf, so kmin <= kmaxf
-    rem = uint32_t(k) - ninf;
-    const uint32_t range = kmaxf - kmin;
-    const int B = range ? 32 - __clz(range) : 0;
-    uint32_t prefix = 0u;   // rel >> hi of the keys still in the running
-    if (B == 0) {
-      cnt = uint32_t(n) - ninf;   // every key below +inf equals kmin
-    } else {
-      int hi = B;
-      bool first = true;
-      while (hi > 0) {
-        const int lo = hi > SD ? hi - SD : 0;
-        const uint32_t dmask = (1u << (hi - lo)) - 1u;
+    int hi = B > SD ? B - SD : 0;
 #pragma unroll
-        for (int j = 0; j < RPT; ++j) {
-          const uint32_t rel = key[j];
-          const uint32_t top = hi >= 32 ? 0u : rel >> hi;
-          if (rel != rinf && top == prefix) atomicAdd(&L.hist[(rel >> lo) & dmask], 1u);
-          __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 32 live masks
-        }
-        __syncthreads();
-        if (wave == 0) {
-          const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
-          if (lane == 0) {
-            L.sh_digit = p.digit;
-            L.sh_rem = p.rem;
-            L.sh_cnt = p.cnt;
-          }
-        }
-        __syncthreads();
-        prefix = (prefix << (hi - lo)) | L.sh_digit;
-        rem = L.sh_rem;
-        cnt = L.sh_cnt;
-        hi = lo;
-        const bool to_list = first && hi > 0 && cnt <= uint32_t(CMAX);
-        if (hi > 0 && !to_list) {
-          // another block-wide digit follows: clear the histogram (the pick above read it
-          // before the barrier that ended it)
-          for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
-          __syncthreads();
-        }
-        if (to_list) {
-          // The `cnt` keys of the chosen bucket (rel >> hi == prefix) go to LDS as their
-          // low hi bits, each thread's after those of the lanes before it.
-          const int Lb = hi;
-          const uint32_t lmask = (1u << Lb) - 1u;
-          uint32_t cmask = 0u;
-#pragma unroll
-          for (int j = 0; j < RPT; ++j)
-            cmask |= uint32_t(key[j] != rinf && (key[j] >> Lb) == prefix) << j;
-          const uint32_t mine = uint32_t(__popc(cmask));
-          const uint32_t incl = wave_incl_scan(mine, lane);
-          uint32_t base = 0u;
-          if (lane == 63) base = atomicAdd(&L.sh_ncand, incl);
-          uint32_t pos = uint32_t(__builtin_amdgcn_readlane(int(base), 63)) + incl - mine;
-#pragma unroll
-          for (int j = 0; j < RPT; ++j) {
-            if ((cmask >> j) & 1u) {
-              if (pos < uint32_t(CMAX)) L.cand[pos] = key[j] & lmask;
-              ++pos;
-            }
-            __builtin_amdgcn_sched_barrier(0);
-          }
-          __syncthreads();
-          if (wave == 0) {
-            // radix passes of WD bits over the list, by this wave alone: its LDS operations
-            // execute in program order, so the clears, the atomics and the reads of whist
-            // need no barrier (the waits and fences keep the compiler from moving them)
-            const int nc = int(min(cnt, uint32_t(CMAX)));
-            uint32_t p2 = 0u, r2 = rem, c2 = cnt;
-            int h2 = Lb;
-            while (h2 > 0) {
-              const int l2 = h2 > WD ? h2 - WD : 0;
-              const uint32_t m2 = (1u << (h2 - l2)) - 1u;
-#pragma unroll
-              for (int q = 0; q < WBINS / 64; ++q) L.whist[WBINS / 64 * lane + q] = 0u;
-              asm volatile("" ::: "memory");
-              // eight reads in flight before their atomics: the list is walked at LDS
-              // throughput rather than one read latency per element
-              for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
-                uint32_t vv[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) vv[u] = L.cand[min(i0 + u * 64 + lane, CMAX - 1)];
-#pragma unroll
-                for (int u = 0; u < 8; ++u)
-                  if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
-                    atomicAdd(&L.whist[(vv[u] >> l2) & m2], 1u);
-              }
-              __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-              asm volatile("" ::: "memory");
-              const Pick pk = pick_bucket<WBINS / 64>(L.whist, r2, lane);
-              __builtin_amdgcn_s_waitcnt(0xc07f);
-              asm volatile("" ::: "memory");
-              p2 = (p2 << (h2 - l2)) | pk.digit;
-              r2 = pk.rem;
-              c2 = pk.cnt;
-              h2 = l2;
-            }
-            if (lane == 0) {
-              L.sh_digit = p2;
-              L.sh_rem = r2;
-              L.sh_cnt = c2;
-            }
-          }
-          __syncthreads();
-          prefix = (prefix << Lb) | L.sh_digit;
-          rem = L.sh_rem;
-          cnt = L.sh_cnt;
-          hi = 0;
-        }
-        first = false;
+    for (int j = 0; j < RPT; ++j) atomicAdd(&L.hist[key[j] >> hi], 1u);
+    __syncthreads();
+    if (wave == 0) {
+      const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
+      if (lane == 0) {
+        L.sh_digit = p.digit;
+        L.sh_rem = p.rem;
+        L.sh_cnt = p.cnt;
       }
     }
-    T = prefix;
-  }
-  // every tie is kept when their count equals the number still to keep (a count that
-  // includes padding cannot: real ties alone already reach rem)
-  const bool all_ties = cnt == rem;
-
-  uint32_t eq = 0u, take = 0u;
+    __syncthreads();
+    prefix = L.sh_digit;
+    rem = L.sh_rem;
+    cnt = L.sh_cnt;
+    if (hi > 0 && cnt <= uint32_t(CMAX)) {
+      // The `cnt` keys of the chosen bucket (rel - cbase < 2^Lb) go to LDS as their low Lb
+      // bits, each thread's after those of the lanes before it; waves holding none skip.
+      const int Lb = hi;
+      const uint32_t cbase = prefix << Lb, width = 1u << Lb;
+      uint32_t dmin = 0xffffffffu;
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    eq |= uint32_t(key[j] == T) << j;
-    take |= uint32_t(key[j] > T) << j;
+      for (int j = 0; j < RPT; ++j) dmin = min(dmin, key[j] - cbase);
+      if (__ballot(dmin < width)) {
+        uint32_t cmask = 0u;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) cmask |= uint32_t(key[j] - cbase < width) << j;
+        const uint32_t mine = uint32_t(__popc(cmask));
+        const uint32_t incl = wave_incl_scan(mine, lane);
+        uint32_t wbase = 0u;
+        if (lane == 63) wbase = atomicAdd(&L.sh_ncand, incl);
+        uint32_t pos = uint32_t(__builtin_amdgcn_readlane(int(wbase), 63)) + incl - mine;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+          if ((cmask >> j) & 1u) {
+            if (pos < uint32_t(CMAX)) L.cand[pos] = key[j] - cbase;
+            ++pos;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // radix passes of WD bits over the list, by this wave alone: its LDS operations
+        // execute in program order, so the clears, the atomics and the reads of whist
+        // need no barrier (the waits and fences keep the compiler from moving them)
+        const int nc = int(min(cnt, uint32_t(CMAX)));
+        uint32_t p2 = 0u, r2 = rem, c2 = cnt;
+        int h2 = Lb;
+        while (h2 > 0) {
+          const int l2 = h2 > WD ? h2 - WD : 0;
+          const uint32_t m2 = (1u << (h2 - l2)) - 1u;
+#pragma unroll
+          for (int q = 0; q < WBINS / 64; ++q) L.whist[WBINS / 64 * lane + q] = 0u;
+          asm volatile("" ::: "memory");
+          // eight reads in flight before their atomics: the list is walked at LDS
+          // throughput rather than one read latency per element
+          for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
+            uint32_t vv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) vv[u] = L.cand[min(i0 + u * 64 + lane, CMAX - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+              if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
+                atomicAdd(&L.whist[(vv[u] >> l2) & m2], 1u);
+          }
+          __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+          asm volatile("" ::: "memory");
+          const Pick pk = pick_bucket<WBINS / 64>(L.whist, r2, lane);
+          __builtin_amdgcn_s_waitcnt(0xc07f);
+          asm volatile("" ::: "memory");
+          p2 = (p2 << (h2 - l2)) | pk.digit;
+          r2 = pk.rem;
+          c2 = pk.cnt;
+          h2 = l2;
+        }
+        if (lane == 0) {
+          L.sh_digit = p2;
+          L.sh_rem = r2;
+          L.sh_cnt = c2;
+        }
+      }
+      __syncthreads();
+      prefix = (prefix << Lb) | L.sh_digit;
+      rem = L.sh_rem;
+      cnt = L.sh_cnt;
+      hi = 0;
+    }
+    while (hi > 0) {
+      // another block-wide digit over the keys whose bits above hi equal prefix: clear the
+      // histogram (the pick above read it before the barrier that ended it)
+      for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
+      __syncthreads();
+      const int lo = hi > SD ? hi - SD : 0;
+      const uint32_t dmask = (1u << (hi - lo)) - 1u;
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) {
+        const uint32_t rel = key[j];
+        if ((rel >> hi) == prefix) atomicAdd(&L.hist[(rel >> lo) & dmask], 1u);
+        __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 32 live masks
+      }
+      __syncthreads();
+      if (wave == 0) {
+        const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
+        if (lane == 0) {
+          L.sh_digit = p.digit;
+          L.sh_rem = p.rem;
+          L.sh_cnt = p.cnt;
+        }
+      }
+      __syncthreads();
+      prefix = (prefix << (hi - lo)) | L.sh_digit;
+      rem = L.sh_rem;
+      cnt = L.sh_cnt;
+      hi = lo;
+    }
   }
+  const uint32_t T = prefix;
+  // every tie is kept when their count equals the number still to keep (a count that
+  // includes padding cannot: real ties alone already reach rem); keys >= T1 are kept
+  // outright
+  const bool all_ties = cnt == rem;
+  const uint32_t T1 = all_ties ? T : T + 1u;
+
+  uint32_t take = 0u;
+#pragma unroll
+  for (int j = RPT - 1; j >= 0; --j) take = (take << 1) | uint32_t(key[j] >= T1);
   uint32_t base[RCH];
-  if (all_ties) {
-    take |= eq;
-  } else {
+  if (!all_ties) {
     // ties ranked in index order; the first rem are kept
+    uint32_t eq = 0u;
+#pragma unroll
+    for (int j = RPT - 1; j >= 0; --j) eq = (eq << 1) | uint32_t(key[j] == T);
     chunk_offsets(eq, base, L.wtot[0], lane, wave);
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
@@ -538,18 +615,26 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
   chunk_offsets(take, base, L.wtot[1], lane, wave);
   int t4s = 4 * tid;
   asm volatile("" : "+v"(t4s));
-  // kept keys of chunk c at ranks base[c], base[c] + 1, ...: stored directly
+  // kept keys of chunk c at ranks base[c], base[c] + 1, ...; the descriptor's bound (the
+  // budget) drops any store past it
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out, 0, 4 * k, 0x00020000);
+  auto emit = [&](auto kept) {
 #pragma unroll
-  for (int c = 0; c < RCH; ++c) {
-    uint32_t r = base[c];
+    for (int c = 0; c < RCH; ++c) {
+      uint32_t r = 4u * base[c];
 #pragma unroll
-    for (int u = 0; u < RCW; ++u) {
-      if ((take >> (RCW * c + u)) & 1u) {
-        out[r] = c * RCHUNK + t4s + u;
-        ++r;
+      for (int u = 0; u < RCW; ++u) {
+        if (kept(RCW * c + u)) {
+          __builtin_amdgcn_raw_buffer_store_b32(uint32_t(c * RCHUNK + t4s + u), rs, int(r), 0, 0);
+          r += 4u;
+        }
       }
     }
-  }
+  };
+  if (all_ties)
+    emit([&](int j) { return key[j] >= T1; });
+  else
+    emit([&](int j) { return ((take >> j) & 1u) != 0u; });
 }
 
 }  // namespace
