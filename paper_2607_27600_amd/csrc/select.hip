@@ -2,8 +2,8 @@
 // come first under (score descending, ties to the lower index), emitted in ascending
 // index order so the compacted cache keeps the original time order.
 //
-// One workgroup per segment.  Scores map to order-preserving 32-bit keys (-0 == +0, NaN
-// below -inf).  8-bit radix passes over the keys (LDS histograms, wave-parallel bucket
+// One workgroup per segment at a time.  Scores map to order-preserving 32-bit keys (-0 ==
+// +0, NaN below -inf).  8-bit radix passes over the keys (LDS histograms, wave-parallel bucket
 // search) find the k-th largest key T and how many entries equal to T are kept; a final
 // pass in index order emits every key > T and the lowest-index ties with block-wide
 // ballot/prefix counts.  Integer work only: the result is exact.  Launches whose longest
@@ -182,9 +182,9 @@ __global__ __launch_bounds__(SNT) void select_keep_kernel(const float* __restric
 //    rel) into a 2048-bin LDS histogram.  An 11-bit digit leaves about an eighth of the keys
 //    an 8-bit one would in the bucket that holds the threshold, and spreads a wave's atomics
 //    over more bins, so fewer lanes of one instruction collide.  When that bucket has at
-//    most CMAX keys, waves that hold any of them copy their low bits to LDS and one wave
-//    finishes the lower digits on that list (9 bits a pass, no block-wide barrier);
-//    otherwise further 11-bit block-wide passes run over the registers.
+//    most CMAX keys, they copy their low bits to LDS (positions from one LDS counter) and
+//    one wave finishes the lower digits on that list (9 bits a pass, no block-wide
+//    barrier); otherwise further 11-bit block-wide passes run over the registers.
 //  - Bucket searches are two-level wave scans: lane sums over the lanes' bin ranges, then
 //    the bins of the lane that holds the rank.
 //  - Emission: a thread's flagged keys per chunk are counted, and one batched scan over
@@ -330,249 +330,156 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
 
 __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restrict__ scores,
                                                            const SelSeg* __restrict__ segs,
-                                                           SelInline inl,
+                                                           SelInline inl, int n_segs,
                                                            int32_t* __restrict__ keep) {
   __shared__ __attribute__((aligned(16))) RegLds L;
-  SelSeg sg = seg_desc(inl, segs, int(blockIdx.x));
-  sg.start = uniform64(sg.start);
-  sg.out = uniform64(sg.out);
-  sg.len = __builtin_amdgcn_readfirstlane(sg.len);
-  sg.k = __builtin_amdgcn_readfirstlane(sg.k);
-  const int n = sg.len, k = sg.k;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  int32_t* out = keep + sg.out;
-  if (k <= 0) return;
-  if (k >= n) {
-    for (int i = tid; i < n; i += RNT) out[i] = i;
-    return;
-  }
-  // key[4c + i] = score c * RCHUNK + 4 * tid + i, read from a uniform base plus a 32-bit
-  // byte offset.  With a 16-byte aligned start and a length divisible by four, one 16-byte
-  // load per chunk (chunks past the end re-read the last four scores); otherwise four
-  // loads per chunk (indices past the end re-read the last score).  Keys past the end are
-  // marked padding below.
-  const char* sb = reinterpret_cast<const char*>(scores + sg.start);
-  uint32_t key[RPT];
-  int t4 = 4 * tid;
-  if ((reinterpret_cast<uintptr_t>(sb) & 15u) == 0u && (n & 3) == 0) {
-#pragma unroll
-    for (int c = 0; c < RCH; ++c) {
-      const uint32_t off = uint32_t(min(c * RCHUNK + t4, n - 4)) * 4u;
-      const uint4 v = *reinterpret_cast<const uint4*>(sb + off);
-      key[4 * c] = v.x;
-      key[4 * c + 1] = v.y;
-      key[4 * c + 2] = v.z;
-      key[4 * c + 3] = v.w;
+  // Workgroups walk the segments (one per CU; the kernel's registers allow no second):
+  // the stores of one segment drain while the loads of the next are in flight.
+  for (int sgi = blockIdx.x; sgi < n_segs; sgi += gridDim.x) {
+    // thread indices opaque per iteration: nothing derived from them is hoisted out of the loop
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    SelSeg sg = seg_desc(inl, segs, sgi);
+    sg.start = uniform64(sg.start);
+    sg.out = uniform64(sg.out);
+    sg.len = __builtin_amdgcn_readfirstlane(sg.len);
+    sg.k = __builtin_amdgcn_readfirstlane(sg.k);
+    const int n = sg.len, k = sg.k;
+    int32_t* out = keep + sg.out;
+    if (k <= 0) continue;
+    if (k >= n) {
+      for (int i = tid; i < n; i += RNT) out[i] = i;
+      continue;
     }
-  } else {
+    // key[4c + i] = score c * RCHUNK + 4 * tid + i, read from a uniform base plus a 32-bit
+    // byte offset.  With a 16-byte aligned start and a length divisible by four, one 16-byte
+    // load per chunk (chunks past the end re-read the last four scores); otherwise four
+    // loads per chunk (indices past the end re-read the last score).  Keys past the end are
+    // marked padding below.
+    const char* sb = reinterpret_cast<const char*>(scores + sg.start);
+    uint32_t key[RPT];
+    int t4 = 4 * tid;
+    if ((reinterpret_cast<uintptr_t>(sb) & 15u) == 0u && (n & 3) == 0) {
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const uint32_t off = uint32_t(min((j >> 2) * RCHUNK + t4 + (j & 3), n - 1)) * 4u;
-      key[j] = *reinterpret_cast<const uint32_t*>(sb + off);
-    }
-  }
-  // Index arithmetic restarts from an opaque copy of 4*tid here and before the stores, so
-  // the compiler recomputes it instead of keeping 64 indices (and their compare masks)
-  // live across the kernel.  vbits: bit j set when key j lies inside the segment.
-  asm volatile("" : "+v"(t4));
-  uint32_t vbits = 0u;
-#pragma unroll
-  for (int c = 0; c < RCH; ++c) {
-    // slots i < n - (c * RCHUNK + 4 tid) of chunk c hold scores
-    const int nv = min(max(n - c * RCHUNK - t4, 0), RCW);
-    vbits |= ((1u << nv) - 1u) << (RCW * c);
-  }
-  const bool whole = vbits == 0xffffffffu;   // every key of this thread lies inside the segment
-  auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
-
-  // keys; their smallest, their largest (NaN detection) and the largest + FIN_SHIFT
-  int32_t mn = I32_MAX, mx = I32_MIN, mf = I32_MIN;
-  if (whole) {
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int32_t s = skey(key[j]);
-      key[j] = uint32_t(s);
-      mn = min(mn, s);
-      mx = max(mx, s);
-      mf = max(mf, int32_t(uint32_t(s) + FIN_SHIFT));
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int32_t s = skey(key[j]);
-      key[j] = uint32_t(s);
-      const bool v = valid(j);
-      mn = v ? min(mn, s) : mn;
-      mx = v ? max(mx, s) : mx;
-      mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
-    }
-  }
-  {
-    const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
-    const uint32_t r1 = wave_reduce(uint32_t(mx), uint32_t(I32_MIN), imax);
-    const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
-    if (lane == 0) {
-      L.red[0][wave] = r0;
-      L.red[1][wave] = r1;
-      L.red[2][wave] = r2;
-    }
-  }
-  for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
-  if (tid == 0) L.sh_ncand = 0u;
-  __syncthreads();
-  mn = int32_t(row0_reduce(lane < RWAVES ? L.red[0][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
-  mx = int32_t(row0_reduce(lane < RWAVES ? L.red[1][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
-  mf = int32_t(row0_reduce(lane < RWAVES ? L.red[2][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
-  if (mn < KEY_NINF || mx > KEY_PINF) {
-    // some score is NaN: every NaN key becomes KEY_NAN and the extremes are taken again
-    // (KEY_NAN + FIN_SHIFT stays clear of INT_MIN)
-    mn = I32_MAX;
-    mf = I32_MIN;
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      int32_t s = int32_t(key[j]);
-      s = (s < KEY_NINF || s > KEY_PINF) ? KEY_NAN : s;
-      key[j] = uint32_t(s);
-      const bool v = valid(j);
-      mn = v ? min(mn, s) : mn;
-      mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
-    }
-    const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
-    const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
-    if (lane == 0) {
-      L.red[3][wave] = r0;
-      L.red[4][wave] = r2;
-    }
-    __syncthreads();
-    mn = int32_t(row0_reduce(lane < RWAVES ? L.red[3][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
-    mf = int32_t(row0_reduce(lane < RWAVES ? L.red[4][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
-  }
-  // From here on the registers hold rel = min(key - kmin, rcap): the order is unchanged and
-  // +inf keys (if any) equal rcap.  With no key below +inf, every rel is 0.  Padding
-  // (indices past the end) becomes rel 0, the smallest key: it is last in index order, and
-  // since k < n the kept ties (lowest index first) never reach it, so it changes no
-  // selection; counts below may include it.
-  const uint32_t kmin = uint32_t(mn);
-  const uint32_t rcap = mf != I32_MIN ? uint32_t(mf) - FIN_SHIFT - kmin + 1u : 0u;
-  if (whole) {
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) key[j] = min(key[j] - kmin, rcap);
-  } else {
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? min(key[j] - kmin, rcap) : 0u;
-  }
-
-  // T: the k-th largest rel; keep `rem` of the keys equal to T, of which there are `cnt`
-  // (a count that may include padding)
-  uint32_t rem = uint32_t(k), cnt;
-  uint32_t prefix = 0u;   // rel >> hi of the keys still in the running
-  const int B = rcap ? 32 - __clz(rcap) : 0;   // rel < 2^B
-  if (B == 0) {
-    cnt = uint32_t(n);   // every key is 0
-  } else {
-    int hi = B > SD ? B - SD : 0;
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) atomicAdd(&L.hist[key[j] >> hi], 1u);
-    __syncthreads();
-    if (wave == 0) {
-      const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
-      if (lane == 0) {
-        L.sh_digit = p.digit;
-        L.sh_rem = p.rem;
-        L.sh_cnt = p.cnt;
+      for (int c = 0; c < RCH; ++c) {
+        const uint32_t off = uint32_t(min(c * RCHUNK + t4, n - 4)) * 4u;
+        const uint4 v = *reinterpret_cast<const uint4*>(sb + off);
+        key[4 * c] = v.x;
+        key[4 * c + 1] = v.y;
+        key[4 * c + 2] = v.z;
+        key[4 * c + 3] = v.w;
       }
-    }
-    __syncthreads();
-    prefix = L.sh_digit;
-    rem = L.sh_rem;
-    cnt = L.sh_cnt;
-    if (hi > 0 && cnt <= uint32_t(CMAX)) {
-      // The `cnt` keys of the chosen bucket (rel - cbase < 2^Lb) go to LDS as their low Lb
-      // bits, each thread's after those of the lanes before it; waves holding none skip.
-      const int Lb = hi;
-      const uint32_t cbase = prefix << Lb, width = 1u << Lb;
-      uint32_t dmin = 0xffffffffu;
-#pragma unroll
-      for (int j = 0; j < RPT; ++j) dmin = min(dmin, key[j] - cbase);
-      if (__ballot(dmin < width)) {
-        uint32_t cmask = 0u;
-#pragma unroll
-        for (int j = 0; j < RPT; ++j) cmask |= uint32_t(key[j] - cbase < width) << j;
-        const uint32_t mine = uint32_t(__popc(cmask));
-        const uint32_t incl = wave_incl_scan(mine, lane);
-        uint32_t wbase = 0u;
-        if (lane == 63) wbase = atomicAdd(&L.sh_ncand, incl);
-        uint32_t pos = uint32_t(__builtin_amdgcn_readlane(int(wbase), 63)) + incl - mine;
-#pragma unroll
-        for (int j = 0; j < RPT; ++j) {
-          if ((cmask >> j) & 1u) {
-            if (pos < uint32_t(CMAX)) L.cand[pos] = key[j] - cbase;
-            ++pos;
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-      __syncthreads();
-      if (wave == 0) {
-        // radix passes of WD bits over the list, by this wave alone: its LDS operations
-        // execute in program order, so the clears, the atomics and the reads of whist
-        // need no barrier (the waits and fences keep the compiler from moving them)
-        const int nc = int(min(cnt, uint32_t(CMAX)));
-        uint32_t p2 = 0u, r2 = rem, c2 = cnt;
-        int h2 = Lb;
-        while (h2 > 0) {
-          const int l2 = h2 > WD ? h2 - WD : 0;
-          const uint32_t m2 = (1u << (h2 - l2)) - 1u;
-#pragma unroll
-          for (int q = 0; q < WBINS / 64; ++q) L.whist[WBINS / 64 * lane + q] = 0u;
-          asm volatile("" ::: "memory");
-          // eight reads in flight before their atomics: the list is walked at LDS
-          // throughput rather than one read latency per element
-          for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
-            uint32_t vv[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) vv[u] = L.cand[min(i0 + u * 64 + lane, CMAX - 1)];
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-              if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
-                atomicAdd(&L.whist[(vv[u] >> l2) & m2], 1u);
-          }
-          __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-          asm volatile("" ::: "memory");
-          const Pick pk = pick_bucket<WBINS / 64>(L.whist, r2, lane);
-          __builtin_amdgcn_s_waitcnt(0xc07f);
-          asm volatile("" ::: "memory");
-          p2 = (p2 << (h2 - l2)) | pk.digit;
-          r2 = pk.rem;
-          c2 = pk.cnt;
-          h2 = l2;
-        }
-        if (lane == 0) {
-          L.sh_digit = p2;
-          L.sh_rem = r2;
-          L.sh_cnt = c2;
-        }
-      }
-      __syncthreads();
-      prefix = (prefix << Lb) | L.sh_digit;
-      rem = L.sh_rem;
-      cnt = L.sh_cnt;
-      hi = 0;
-    }
-    while (hi > 0) {
-      // another block-wide digit over the keys whose bits above hi equal prefix: clear the
-      // histogram (the pick above read it before the barrier that ended it)
-      for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
-      __syncthreads();
-      const int lo = hi > SD ? hi - SD : 0;
-      const uint32_t dmask = (1u << (hi - lo)) - 1u;
+    } else {
 #pragma unroll
       for (int j = 0; j < RPT; ++j) {
-        const uint32_t rel = key[j];
-        if ((rel >> hi) == prefix) atomicAdd(&L.hist[(rel >> lo) & dmask], 1u);
-        __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 32 live masks
+        const uint32_t off = uint32_t(min((j >> 2) * RCHUNK + t4 + (j & 3), n - 1)) * 4u;
+        key[j] = *reinterpret_cast<const uint32_t*>(sb + off);
       }
+    }
+    // Index arithmetic restarts from an opaque copy of 4*tid here and before the stores, so
+    // the compiler recomputes it instead of keeping 64 indices (and their compare masks)
+    // live across the kernel.  vbits: bit j set when key j lies inside the segment.
+    asm volatile("" : "+v"(t4));
+    uint32_t vbits = 0u;
+#pragma unroll
+    for (int c = 0; c < RCH; ++c) {
+      // slots i < n - (c * RCHUNK + 4 tid) of chunk c hold scores
+      const int nv = min(max(n - c * RCHUNK - t4, 0), RCW);
+      vbits |= ((1u << nv) - 1u) << (RCW * c);
+    }
+    const bool whole = vbits == 0xffffffffu;   // every key of this thread lies inside the segment
+    auto valid = [&](int j) { return ((vbits >> j) & 1u) != 0u; };
+
+    // keys; their smallest, their largest (NaN detection) and the largest + FIN_SHIFT
+    int32_t mn = I32_MAX, mx = I32_MIN, mf = I32_MIN;
+    if (whole) {
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) {
+        const int32_t s = skey(key[j]);
+        key[j] = uint32_t(s);
+        mn = min(mn, s);
+        mx = max(mx, s);
+        mf = max(mf, int32_t(uint32_t(s) + FIN_SHIFT));
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) {
+        const int32_t s = skey(key[j]);
+        key[j] = uint32_t(s);
+        const bool v = valid(j);
+        mn = v ? min(mn, s) : mn;
+        mx = v ? max(mx, s) : mx;
+        mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
+      }
+    }
+    {
+      const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
+      const uint32_t r1 = wave_reduce(uint32_t(mx), uint32_t(I32_MIN), imax);
+      const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
+      if (lane == 0) {
+        L.red[0][wave] = r0;
+        L.red[1][wave] = r1;
+        L.red[2][wave] = r2;
+      }
+    }
+    for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
+    if (tid == 0) L.sh_ncand = 0u;
+    __syncthreads();
+    mn = int32_t(row0_reduce(lane < RWAVES ? L.red[0][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
+    mx = int32_t(row0_reduce(lane < RWAVES ? L.red[1][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
+    mf = int32_t(row0_reduce(lane < RWAVES ? L.red[2][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
+    if (mn < KEY_NINF || mx > KEY_PINF) {
+      // some score is NaN: every NaN key becomes KEY_NAN and the extremes are taken again
+      // (KEY_NAN + FIN_SHIFT stays clear of INT_MIN)
+      mn = I32_MAX;
+      mf = I32_MIN;
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) {
+        int32_t s = int32_t(key[j]);
+        s = (s < KEY_NINF || s > KEY_PINF) ? KEY_NAN : s;
+        key[j] = uint32_t(s);
+        const bool v = valid(j);
+        mn = v ? min(mn, s) : mn;
+        mf = v ? max(mf, int32_t(uint32_t(s) + FIN_SHIFT)) : mf;
+      }
+      const uint32_t r0 = wave_reduce(uint32_t(mn), uint32_t(I32_MAX), imin);
+      const uint32_t r2 = wave_reduce(uint32_t(mf), uint32_t(I32_MIN), imax);
+      if (lane == 0) {
+        L.red[3][wave] = r0;
+        L.red[4][wave] = r2;
+      }
+      __syncthreads();
+      mn = int32_t(row0_reduce(lane < RWAVES ? L.red[3][lane] : uint32_t(I32_MAX), uint32_t(I32_MAX), imin));
+      mf = int32_t(row0_reduce(lane < RWAVES ? L.red[4][lane] : uint32_t(I32_MIN), uint32_t(I32_MIN), imax));
+    }
+    // From here on the registers hold rel = min(key - kmin, rcap): the order is unchanged and
+    // +inf keys (if any) equal rcap.  With no key below +inf, every rel is 0.  Padding
+    // (indices past the end) becomes rel 0, the smallest key: it is last in index order, and
+    // since k < n the kept ties (lowest index first) never reach it, so it changes no
+    // selection; counts below may include it.
+    const uint32_t kmin = uint32_t(mn);
+    const uint32_t rcap = mf != I32_MIN ? uint32_t(mf) - FIN_SHIFT - kmin + 1u : 0u;
+    if (whole) {
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) key[j] = min(key[j] - kmin, rcap);
+    } else {
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) key[j] = valid(j) ? min(key[j] - kmin, rcap) : 0u;
+    }
+
+    // T: the k-th largest rel; keep `rem` of the keys equal to T, of which there are `cnt`
+    // (a count that may include padding)
+    uint32_t rem = uint32_t(k), cnt;
+    uint32_t prefix = 0u;   // rel >> hi of the keys still in the running
+    const int B = rcap ? 32 - __clz(rcap) : 0;   // rel < 2^B
+    if (B == 0) {
+      cnt = uint32_t(n);   // every key is 0
+    } else {
+      int hi = B > SD ? B - SD : 0;
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) atomicAdd(&L.hist[key[j] >> hi], 1u);
       __syncthreads();
       if (wave == 0) {
         const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
@@ -583,58 +490,147 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
         }
       }
       __syncthreads();
-      prefix = (prefix << (hi - lo)) | L.sh_digit;
+      prefix = L.sh_digit;
       rem = L.sh_rem;
       cnt = L.sh_cnt;
-      hi = lo;
-    }
-  }
-  const uint32_t T = prefix;
-  // every tie is kept when their count equals the number still to keep (a count that
-  // includes padding cannot: real ties alone already reach rem); keys >= T1 are kept
-  // outright
-  const bool all_ties = cnt == rem;
-  const uint32_t T1 = all_ties ? T : T + 1u;
-
-  uint32_t take = 0u;
+      if (hi > 0 && cnt <= uint32_t(CMAX)) {
+        // The `cnt` keys of the chosen bucket (rel - cbase < 2^Lb) go to LDS as their low Lb
+        // bits.
+        const int Lb = hi;
+        const uint32_t cbase = prefix << Lb, width = 1u << Lb;
 #pragma unroll
-  for (int j = RPT - 1; j >= 0; --j) take = (take << 1) | uint32_t(key[j] >= T1);
-  uint32_t base[RCH];
-  if (!all_ties) {
-    // ties ranked in index order; the first rem are kept
-    uint32_t eq = 0u;
-#pragma unroll
-    for (int j = RPT - 1; j >= 0; --j) eq = (eq << 1) | uint32_t(key[j] == T);
-    chunk_offsets(eq, base, L.wtot[0], lane, wave);
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const uint32_t below = uint32_t(__popc(eq & (((1u << (j & 3)) - 1u) << (j & ~3))));
-      take |= uint32_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
-    }
-  }
-  chunk_offsets(take, base, L.wtot[1], lane, wave);
-  int t4s = 4 * tid;
-  asm volatile("" : "+v"(t4s));
-  // kept keys of chunk c at ranks base[c], base[c] + 1, ...; the descriptor's bound (the
-  // budget) drops any store past it
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out, 0, 4 * k, 0x00020000);
-  auto emit = [&](auto kept) {
-#pragma unroll
-    for (int c = 0; c < RCH; ++c) {
-      uint32_t r = 4u * base[c];
-#pragma unroll
-      for (int u = 0; u < RCW; ++u) {
-        if (kept(RCW * c + u)) {
-          __builtin_amdgcn_raw_buffer_store_b32(uint32_t(c * RCHUNK + t4s + u), rs, int(r), 0, 0);
-          r += 4u;
+        for (int j = 0; j < RPT; ++j) {
+          // a key enters the list where it finds it (the finish needs no order); the
+          // increments of one instruction are combined by a single lane
+          const uint32_t d = key[j] - cbase;
+          if (d < width) {
+            const uint32_t pos = atomicAdd(&L.sh_ncand, 1u);
+            if (pos < uint32_t(CMAX)) L.cand[pos] = d;
+          }
         }
+        __syncthreads();
+        if (wave == 0) {
+          // radix passes of WD bits over the list, by this wave alone: its LDS operations
+          // execute in program order, so the clears, the atomics and the reads of whist
+          // need no barrier (the waits and fences keep the compiler from moving them)
+          const int nc = int(min(cnt, uint32_t(CMAX)));
+          uint32_t p2 = 0u, r2 = rem, c2 = cnt;
+          int h2 = Lb;
+          while (h2 > 0) {
+            const int l2 = h2 > WD ? h2 - WD : 0;
+            const uint32_t m2 = (1u << (h2 - l2)) - 1u;
+#pragma unroll
+            for (int q = 0; q < WBINS / 64; ++q) L.whist[WBINS / 64 * lane + q] = 0u;
+            asm volatile("" ::: "memory");
+            // eight reads in flight before their atomics: the list is walked at LDS
+            // throughput rather than one read latency per element
+            for (int i0 = 0; i0 < nc; i0 += 8 * 64) {
+              uint32_t vv[8];
+#pragma unroll
+              for (int u = 0; u < 8; ++u) vv[u] = L.cand[min(i0 + u * 64 + lane, CMAX - 1)];
+#pragma unroll
+              for (int u = 0; u < 8; ++u)
+                if (i0 + u * 64 + lane < nc && (vv[u] >> h2) == p2)
+                  atomicAdd(&L.whist[(vv[u] >> l2) & m2], 1u);
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+            asm volatile("" ::: "memory");
+            const Pick pk = pick_bucket<WBINS / 64>(L.whist, r2, lane);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            asm volatile("" ::: "memory");
+            p2 = (p2 << (h2 - l2)) | pk.digit;
+            r2 = pk.rem;
+            c2 = pk.cnt;
+            h2 = l2;
+          }
+          if (lane == 0) {
+            L.sh_digit = p2;
+            L.sh_rem = r2;
+            L.sh_cnt = c2;
+          }
+        }
+        __syncthreads();
+        prefix = (prefix << Lb) | L.sh_digit;
+        rem = L.sh_rem;
+        cnt = L.sh_cnt;
+        hi = 0;
+      }
+      while (hi > 0) {
+        // another block-wide digit over the keys whose bits above hi equal prefix: clear the
+        // histogram (the pick above read it before the barrier that ended it)
+        for (int i = tid; i < SBINS; i += RNT) L.hist[i] = 0u;
+        __syncthreads();
+        const int lo = hi > SD ? hi - SD : 0;
+        const uint32_t dmask = (1u << (hi - lo)) - 1u;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+          const uint32_t rel = key[j];
+          if ((rel >> hi) == prefix) atomicAdd(&L.hist[(rel >> lo) & dmask], 1u);
+          __builtin_amdgcn_sched_barrier(0);   // one key at a time: no 32 live masks
+        }
+        __syncthreads();
+        if (wave == 0) {
+          const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
+          if (lane == 0) {
+            L.sh_digit = p.digit;
+            L.sh_rem = p.rem;
+            L.sh_cnt = p.cnt;
+          }
+        }
+        __syncthreads();
+        prefix = (prefix << (hi - lo)) | L.sh_digit;
+        rem = L.sh_rem;
+        cnt = L.sh_cnt;
+        hi = lo;
       }
     }
-  };
-  if (all_ties)
-    emit([&](int j) { return key[j] >= T1; });
-  else
-    emit([&](int j) { return ((take >> j) & 1u) != 0u; });
+    const uint32_t T = prefix;
+    // every tie is kept when their count equals the number still to keep (a count that
+    // includes padding cannot: real ties alone already reach rem); keys >= T1 are kept
+    // outright
+    const bool all_ties = cnt == rem;
+    const uint32_t T1 = all_ties ? T : T + 1u;
+
+    uint32_t take = 0u;
+#pragma unroll
+    for (int j = RPT - 1; j >= 0; --j) take = (take << 1) | uint32_t(key[j] >= T1);
+    uint32_t base[RCH];
+    if (!all_ties) {
+      // ties ranked in index order; the first rem are kept
+      uint32_t eq = 0u;
+#pragma unroll
+      for (int j = RPT - 1; j >= 0; --j) eq = (eq << 1) | uint32_t(key[j] == T);
+      chunk_offsets(eq, base, L.wtot[0], lane, wave);
+#pragma unroll
+      for (int j = 0; j < RPT; ++j) {
+        const uint32_t below = uint32_t(__popc(eq & (((1u << (j & 3)) - 1u) << (j & ~3))));
+        take |= uint32_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
+      }
+    }
+    chunk_offsets(take, base, L.wtot[1], lane, wave);
+    int t4s = 4 * tid;
+    asm volatile("" : "+v"(t4s));
+    // kept keys of chunk c at ranks base[c], base[c] + 1, ...; the descriptor's bound (the
+    // budget) drops any store past it
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out, 0, 4 * k, 0x00020000);
+    auto emit = [&](auto kept) {
+#pragma unroll
+      for (int c = 0; c < RCH; ++c) {
+        uint32_t r = 4u * base[c];
+#pragma unroll
+        for (int u = 0; u < RCW; ++u) {
+          if (kept(RCW * c + u)) {
+            __builtin_amdgcn_raw_buffer_store_b32(uint32_t(c * RCHUNK + t4s + u), rs, int(r), 0, 0);
+            r += 4u;
+          }
+        }
+      }
+    };
+    if (all_ties)
+      emit([&](int j) { return key[j] >= T1; });
+    else
+      emit([&](int j) { return ((take >> j) & 1u) != 0u; });
+  }
 }
 
 }  // namespace
@@ -668,10 +664,17 @@ hipError_t launch_select(const float* scores, const SelSeg* segs_h, const SelSeg
   // The register path pays a fixed cost per segment (its passes and scans are a chain of
   // block-wide barriers) that the re-reading kernel does not; it wins once a segment is
   // long enough for the repeated reads to dominate.
-  if (max_len > 8192 && max_len <= RMAX)
-    hipLaunchKernelGGL(select_keep_regs, dim3(n_segs), dim3(RNT), 0, s, scores, segs_d, inl, keep);
-  else
+  if (max_len > 8192 && max_len <= RMAX) {
+    // one workgroup per CU of the current device, each walking segments
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(select_keep_regs, dim3(std::min(n_segs, std::max(cus, 1))), dim3(RNT), 0, s, scores,
+                       segs_d, inl, n_segs, keep);
+  } else {
     hipLaunchKernelGGL(select_keep_kernel, dim3(n_segs), dim3(SNT), 0, s, scores, segs_d, inl, keep);
+  }
   return hipGetLastError();
 }
 

@@ -211,6 +211,52 @@ def test_select_many_long_segments_mixed_branches():
         off += k
 
 
+def test_select_thousands_of_long_segments():
+    """Over 2048 long segments (eight workgroups of the register path per CU): unaligned
+    starts, lengths not divisible by four, k = 0 and k = len next to ordinary budgets, five
+    score distributions.  Every fifth pair of neighbours and the last segment against the
+    oracle; every list ascending and inside its segment."""
+    r = np.random.default_rng(77)
+    n_segs = 2049
+    lens = [int(x) for x in r.choice([8196, 9000, 12288, 16384, 32768, 8193, 10001], n_segs)]
+    segs, ks, starts, pos = [], [], [], 0
+    for i, n in enumerate(lens):
+        kind = i % 5
+        if kind == 0:
+            x = r.exponential(3.0, n)
+            x[-1] = np.inf
+        elif kind == 1:
+            x = 11.0 + r.uniform(0.0, 1e-4, n)
+        elif kind == 2:
+            x = 1.0 + r.integers(0, 300, n) * 2.0 ** -23
+        elif kind == 3:
+            x = np.round(r.standard_normal(n), 2)
+            x[::17] = -np.inf
+        else:
+            x = r.exponential(3.0, n)
+            x[r.permutation(n)[: n // 3]] = np.inf
+        pos += 1 if i % 7 == 3 else 0   # a 4-byte offset: an unaligned start
+        starts.append(pos)
+        segs.append((pos, np.asarray(x, dtype=np.float32)))
+        pos += n
+        ks.append(int(r.choice([0, 1, n // 4, n // 4, n // 2, n - 1, n])))
+    s = np.zeros(pos, dtype=np.float32)
+    for st, x in segs:
+        s[st:st + len(x)] = x
+    print(f"[select] two per workgroup: {n_segs} segments, {len(s)} scores", flush=True)
+    got = _gpu_select(s, starts, lens, ks)
+    offs = np.concatenate([[0], np.cumsum(ks)])
+    check = sorted({i for w in range(0, n_segs // 2 + 1, 5) for i in (2 * w, 2 * w + 1) if i < n_segs}
+                   | {n_segs - 1})
+    for i in range(n_segs):
+        g = got[offs[i]:offs[i + 1]]
+        assert len(g) == 0 or (g[0] >= 0 and g[-1] < lens[i] and np.all(np.diff(g) > 0)), f"segment {i}"
+    for i in check:
+        st, n, k = starts[i], lens[i], ks[i]
+        np.testing.assert_array_equal(got[offs[i]:offs[i + 1]], O.select_keep(s[st:st + n], k),
+                                      err_msg=f"segment {i} len={n} k={k}")
+
+
 def test_select_overlapping_segments_identical_lists():
     r = np.random.default_rng(9)
     s = r.standard_normal(4096).astype(np.float32)
