@@ -276,19 +276,18 @@ __device__ __forceinline__ Pick pick_bucket(const uint32_t* h, uint32_t rem, int
   return {uint32_t(top - j), rem - before - (ij - cj), cj};
 }
 
-// Ranks in index order of the keys flagged in m (bit 4c + i: slot i of chunk c): base[c]
-// = flagged keys before this thread's part of chunk c.  wtot: [RWAVES][RCH / 2] words of
+// Ranks in index order of flagged keys: base[c] = flagged keys before this thread's part of
+// chunk c.  wtot: [RWAVES][RCH / 2] words of
 // LDS owned by this call (16-byte aligned rows); wave: the wave's index, uniform.  Contains
 // one barrier.  After it, lanes 0..15 of every wave scan the 16 waves' totals.
 static_assert(RPT == 32, "one bit per key in a 32-bit mask");
 static_assert(RWAVES == 16, "the waves' totals are combined in one row of 16 lanes");
-__device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
+// own[q]: this thread's flagged keys in chunks 2q (low half) and 2q + 1 (high half).
+__device__ __forceinline__ void chunk_offsets(const uint32_t (&own)[RCH / 2], uint32_t (&base)[RCH],
                                               uint32_t (*wtot)[RCH / 2], int lane, int wave) {
-  uint32_t own[RCH / 2], inc[RCH / 2];
+  uint32_t inc[RCH / 2];
 #pragma unroll
   for (int q = 0; q < RCH / 2; ++q) {
-    own[q] = uint32_t(__popc((m >> (8 * q)) & 0xfu)) |
-             (uint32_t(__popc((m >> (8 * q + 4)) & 0xfu)) << 16);
     // inclusive scan over the wave, two chunks per word (a field stays below 4 * 64 + 1)
     inc[q] = wave_incl_scan(own[q], lane);
   }
@@ -309,6 +308,13 @@ __device__ __forceinline__ void chunk_offsets(uint32_t m, uint32_t (&base)[RCH],
     base[2 * q + 1] = run + (mine >> 16);
     run += all >> 16;
   }
+}
+
+// own[] of chunk_offsets from a mask (bit 4c + i: slot i of chunk c)
+__device__ __forceinline__ void chunk_counts(uint32_t m, uint32_t (&own)[RCH / 2]) {
+#pragma unroll
+  for (int q = 0; q < RCH / 2; ++q)
+    own[q] = uint32_t(__popc((m >> (8 * q)) & 0xfu)) | (uint32_t(__popc((m >> (8 * q + 4)) & 0xfu)) << 16);
 }
 
 struct RegLds {
@@ -591,23 +597,37 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
     const bool all_ties = cnt == rem;
     const uint32_t T1 = all_ties ? T : T + 1u;
 
-    uint32_t take = 0u;
-#pragma unroll
-    for (int j = RPT - 1; j >= 0; --j) take = (take << 1) | uint32_t(key[j] >= T1);
+    uint32_t take = 0u, own[RCH / 2];
     uint32_t base[RCH];
-    if (!all_ties) {
+    if (all_ties) {
+      // kept: the keys >= T1, counted per chunk (no mask: the stores compare again)
+      uint32_t cc[RCH];
+#pragma unroll
+      for (int c = 0; c < RCH; ++c) {
+        cc[c] = 0u;
+#pragma unroll
+        for (int u = 0; u < RCW; ++u) cc[c] += uint32_t(key[RCW * c + u] >= T1);
+      }
+#pragma unroll
+      for (int q = 0; q < RCH / 2; ++q) own[q] = cc[2 * q] | (cc[2 * q + 1] << 16);
+    } else {
       // ties ranked in index order; the first rem are kept
       uint32_t eq = 0u;
 #pragma unroll
-      for (int j = RPT - 1; j >= 0; --j) eq = (eq << 1) | uint32_t(key[j] == T);
-      chunk_offsets(eq, base, L.wtot[0], lane, wave);
+      for (int j = RPT - 1; j >= 0; --j) {
+        take = (take << 1) | uint32_t(key[j] >= T1);
+        eq = (eq << 1) | uint32_t(key[j] == T);
+      }
+      chunk_counts(eq, own);
+      chunk_offsets(own, base, L.wtot[0], lane, wave);
 #pragma unroll
       for (int j = 0; j < RPT; ++j) {
         const uint32_t below = uint32_t(__popc(eq & (((1u << (j & 3)) - 1u) << (j & ~3))));
         take |= uint32_t(((eq >> j) & 1u) && base[j >> 2] + below < rem) << j;
       }
+      chunk_counts(take, own);
     }
-    chunk_offsets(take, base, L.wtot[1], lane, wave);
+    chunk_offsets(own, base, L.wtot[1], lane, wave);
     int t4s = 4 * tid;
     asm volatile("" : "+v"(t4s));
     // kept keys of chunk c at ranks base[c], base[c] + 1, ...; the descriptor's bound (the
