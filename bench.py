@@ -588,7 +588,7 @@ def bench_loop(args, dev) -> dict:
     SwiGLU 18944, vocab 152064) in the exact fast variant: a 4096-token prompt appended in
     chunks, then 1024 decoded tokens appended one at a time, a refresh every 256 tokens
     (each scores J + h = 768 entries).  Keys, values, activations and ids of the stream
-    are seeded synthetic data; the inference cycle itself is not part of this build, so
+    are seeded synthetic data; the model forward that produces them lies outside this library, so
     appends are copies of the stream's next entries."""
     import numpy as np
     import torch

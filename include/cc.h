@@ -49,7 +49,7 @@ typedef enum cc_status {
   CC_ERR_SHAPE = 2,        /* inconsistent sizes (e.g. n_heads_q % n_heads_kv != 0) */
   CC_ERR_DTYPE = 3,        /* dtype not valid for this call */
   CC_ERR_WORKSPACE = 4,    /* workspace smaller than the query returned */
-  CC_ERR_UNSUPPORTED = 5,  /* a valid problem this build has no kernel for */
+  CC_ERR_UNSUPPORTED = 5,  /* a valid problem this library has no kernel for */
   CC_ERR_HIP = 6,          /* the HIP runtime rejected a launch or copy */
   CC_ERR_SCRATCH = 7       /* the call needs more than the static scratch of the
                               allocation-free entry point holds */
