@@ -223,28 +223,31 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   auto slab_of = [&](int i) {
     return RPW * NWAVES > 16 ? (RPW * NWAVES / 16) * i + (RPW * wave_u) / 16 : i;
   };
+  // Page numbers of this wave's slabs of tile t (paged caches; K and V share the block
+  // table): scalar loads, waited for at once.  Slabs past the sequence end take its last page.
+  auto load_pages = [&](int t, int (&pg)[NI]) {
+    if constexpr (PAGED) {
+      const int32_t* pp[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) pp[i] = btab + min((t * BN + 16 * slab_of(i)) >> a.k.page_shift, last_page);
+      if constexpr (NI == 4)
+        page_numbers(pp[0], pp[1], pp[2], pp[3], pg[0], pg[1], pg[2], pg[3]);
+      else
+        page_numbers(pp[0], pp[1], pg[0], pg[1]);
+    }
+  };
   // Fill an LDS tile with tile t.  Full tiles of a contiguous cache: from a running tile
   // pointer (tile_ptr = plane + t * BN keys, advanced once per tile), a 64-bit scalar add per
   // 16-key slab and the lane's fixed offset.  Full tiles of a paged cache: a uniform base per
-  // slab from its page.  The last, partial tile: per-lane rows (clamped), per-lane page
-  // lookups.
+  // slab from its page, pg (loaded beforehand by load_pages).  The last, partial tile:
+  // per-lane rows (clamped), per-lane page lookups.
   auto issue = [&](u16* dst, int t, const KvView& kv, const char* plane, const char* tile_ptr,
-                   uint32_t lane_off, int ch, int64_t ts) {
+                   uint32_t lane_off, int ch, int64_t ts, const int (&pg)[NI]) {
     const int key0 = t * BN;
     u16* lds = dst + wave_u * RPW * HD;
     if (key0 + BN <= n) {
       // keep the 32-bit offset opaque here so that it is not widened outside the loop
       asm volatile("" : "+v"(lane_off));
-      int pg[NI];
-      if constexpr (PAGED) {
-        const int32_t* pp[NI];
-#pragma unroll
-        for (int i = 0; i < NI; ++i) pp[i] = btab + min((key0 + 16 * slab_of(i)) >> kv.page_shift, last_page);
-        if constexpr (NI == 4)
-          page_numbers(pp[0], pp[1], pp[2], pp[3], pg[0], pg[1], pg[2], pg[3]);
-        else
-          page_numbers(pp[0], pp[1], pg[0], pg[1]);
-      }
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int si = slab_of(i);
@@ -338,10 +341,17 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
   const int64_t kstep = int64_t(BN) * kts, vstep = int64_t(BN) * vts;
   const char* kptr = kplane + int64_t(tb + 2) * kstep;
   const char* vptr = vplane + int64_t(tb + 1) * vstep;
+  // Paged caches: the page numbers of the tiles the next step loads are fetched at the end
+  // of the step before (a tile's K pages are the next step's V pages), so no step waits for
+  // a scalar load before its DMAs.  kpg: pages of tile t + 2 (K), vpg: of tile t + 1 (V).
+  int kpg[NI], vpg[NI];
   // prologue: K(tb), V(tb), K(tb+1) in LDS; S(tb) and its unmasked row max in registers.
-  issue(kl0, tb, a.k, kplane, kplane + int64_t(tb) * kstep, klane, kch, kts);
-  issue(vl0, tb, a.v, vplane, vplane + int64_t(tb) * vstep, vlane, vch, vts);
-  if (tb + 1 < te) issue(kl1, tb + 1, a.k, kplane, kplane + int64_t(tb + 1) * kstep, klane, kch, kts);
+  load_pages(tb, kpg);
+  issue(kl0, tb, a.k, kplane, kplane + int64_t(tb) * kstep, klane, kch, kts, kpg);
+  issue(vl0, tb, a.v, vplane, vplane + int64_t(tb) * vstep, vlane, vch, vts, kpg);
+  load_pages(tb + 1, vpg);
+  if (tb + 1 < te) issue(kl1, tb + 1, a.k, kplane, kplane + int64_t(tb + 1) * kstep, klane, kch, kts, vpg);
+  if (tb + 2 < te) load_pages(tb + 2, kpg);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   f32x16 sa[2], sb[2];
@@ -365,8 +375,8 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     const u16* Vc = P ? vl1 : vl0;
     u16* Vfree = P ? vl0 : vl1;
     // tiles past the last are never read: nothing to load
-    if (t + 2 < te) issue(Kfree, t + 2, a.k, kplane, kptr, klane, kch, kts);
-    if (t + 1 < te) issue(Vfree, t + 1, a.v, vplane, vptr, vlane, vch, vts);
+    if (t + 2 < te) issue(Kfree, t + 2, a.k, kplane, kptr, klane, kch, kts, kpg);
+    if (t + 1 < te) issue(Vfree, t + 1, a.v, vplane, vptr, vlane, vch, vts, vpg);
     kptr += kstep;
     vptr += vstep;
     bf16x8 kf[4];
@@ -470,6 +480,13 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
     }
     l_run = l_run * corr + (ls0 + ls1);
     mx = half_max(fmaxf(m0, m1));
+    if constexpr (PAGED) {
+      // pages of the next step's tiles; no LDS read is outstanding here, so the loads' wait
+      // overlaps the DMA wait below
+#pragma unroll
+      for (int i = 0; i < NI; ++i) vpg[i] = kpg[i];
+      if (t + 3 < te) load_pages(t + 3, kpg);
+    }
     __builtin_amdgcn_s_waitcnt(0);   // this wave's DMAs have landed
     __syncthreads();                 // everyone's, and everyone is done with K(t+1), V(t)
   };
