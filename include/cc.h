@@ -103,7 +103,9 @@ typedef struct cc_kv {
   int64_t layer_stride;
   int64_t head_stride;
   int64_t tok_stride;
-  int64_t page_stride;         /* PAGED only */
+  int64_t page_stride;         /* PAGED only: one page spans less than 4 GiB, i.e.
+                                  page_stride and page_size*tok_stride, in bytes, are
+                                  below 2^32 (CC_ERR_UNSUPPORTED otherwise) */
   const int32_t* block_table;  /* PAGED only: device [n_seqs][max_pages] page ids */
   int32_t page_size;           /* PAGED only: tokens per page, a power of two >= 16 */
   int32_t max_pages;           /* PAGED only: row length of block_table */

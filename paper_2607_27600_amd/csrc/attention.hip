@@ -245,6 +245,7 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
                    uint32_t lane_off, int ch, int64_t ts, const int (&pg)[NI]) {
     const int key0 = t * BN;
     u16* lds = dst + wave_u * RPW * HD;
+    const uint32_t pstride = uint32_t(kv.page_stride * 2);   // bytes per page
     if (key0 + BN <= n) {
       // keep the 32-bit offset opaque here so that it is not widened outside the loop
       asm volatile("" : "+v"(lane_off));
@@ -252,9 +253,9 @@ __global__ __launch_bounds__(256, 2) void attn_cc_bf16(AttnArgs a) {
       for (int i = 0; i < NI; ++i) {
         const int si = slab_of(i);
         const char* base;
-        if constexpr (PAGED)
-          base = uniform_ptr(plane + (int64_t(pg[i]) * kv.page_stride +
-                                      int64_t((key0 + 16 * si) & kv.page_mask) * kv.tok_stride) * 2);
+        if constexpr (PAGED)   // a page spans < 4 GiB: 32 x 32 -> 64-bit page offset
+          base = uniform_ptr(plane + (uint64_t(uint32_t(pg[i])) * pstride +
+                                      uint32_t((key0 + 16 * si) & kv.page_mask) * uint32_t(ts)));
         else
           base = tile_ptr + int64_t(16 * si) * ts;
         dma16(base, lane_off, lds_addr(lds + i * NWAVES * RPW * HD));

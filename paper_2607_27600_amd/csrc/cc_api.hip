@@ -84,6 +84,10 @@ cc_status check_kv(const cc_problem* p, const cc_kv* kv, int min_layers) {
   if (kv->layout == CC_KV_PAGED) {
     if (!kv->block_table || !is_pow2(kv->page_size) || kv->page_size < 16) return CC_ERR_ARG;
     if (kv->page_stride < 0 || !str_ok(kv->page_stride)) return CC_ERR_UNSUPPORTED;
+    // in-page byte offsets are 32-bit in the kernels
+    constexpr int64_t kPageLimit = int64_t(1) << 32;
+    if (kv->page_stride * es >= kPageLimit || int64_t(kv->page_size) * kv->tok_stride * es >= kPageLimit)
+      return CC_ERR_UNSUPPORTED;
     const int need = (max_len(p) + kv->page_size - 1) / kv->page_size;
     if (kv->max_pages < need) return CC_ERR_SHAPE;
   } else {

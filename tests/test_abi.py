@@ -112,6 +112,17 @@ def test_calls_with_bad_arguments_enqueue_nothing():
     kv = cc.c_kv()
     assert lib.cc_attention_cc(ctypes.byref(p), None, ctypes.byref(kv), 0, None, None, 0,
                                None) == cc.CC_ERR_ARG
+    # a paged view whose page spans 4 GiB or more is refused (in-page offsets are 32-bit)
+    kvp = cc.c_kv()
+    kvp.layout, kvp.n_layers = cc.CC_KV_PAGED, 1
+    kvp.k = kvp.v = 0x10000                       # 16-byte aligned, never dereferenced
+    kvp.head_stride, kvp.tok_stride, kvp.page_size, kvp.max_pages = 16 * 128, 128, 16, 16
+    kvp.block_table = 0x10000
+    dummy16 = ctypes.c_void_p(0x10000)
+    for page_stride, want in (((1 << 31), cc.CC_ERR_UNSUPPORTED), ((1 << 31) - 8, cc.CC_ERR_WORKSPACE)):
+        kvp.page_stride = page_stride                # elements: x2 bytes reaches 2^32 or not
+        assert lib.cc_attention_cc(ctypes.byref(p), dummy16, ctypes.byref(kvp), 0, dummy16, None, 0,
+                                   None) == want
     st = (ctypes.c_int64 * 1)(0)
     ln = (ctypes.c_int32 * 1)(10)
     kk = (ctypes.c_int32 * 1)(11)                   # k > len
