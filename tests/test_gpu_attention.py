@@ -106,6 +106,17 @@ def test_bf16_head_dim_64_ragged_batch_gqa7():
     _check(got, ref, "bf16", "d=64 gqa7")
 
 
+@pytest.mark.parametrize("page_size", [32, 64])
+def test_bf16_paged_larger_pages(page_size):
+    """Pages of 32 and 64 keys: a 16-key slab then starts inside its page, at a nonzero
+    in-page offset (head_dim 128 and 64)."""
+    for hd in (128, 64):
+        cfg = C.shrink(C.C5, seq_lens=(17, 100, 300, 16), head_dim=hd, cache_layers=1,
+                       keep=(1, 1, 1, 1), page_size=page_size)
+        got, ref, _ = _run(cfg)
+        _check(got, ref, "bf16", f"P={page_size} d={hd}")
+
+
 def test_bf16_head_dim_64_paged_and_mha():
     cfg = C.shrink(C.C5, seq_lens=(17, 100, 260, 16), head_dim=64, cache_layers=1,
                    keep=(1, 1, 1, 1))
