@@ -484,8 +484,16 @@ __global__ __launch_bounds__(RNT, 1) void select_keep_regs(const float* __restri
       cnt = uint32_t(n);   // every key is 0
     } else {
       int hi = B > SD ? B - SD : 0;
+      // Chunks wholly past the end hold only padding (rel 0): one thread counts them into
+      // bin 0 at once.  Key by key, every lane of such a load's keys would hit that one bin.
 #pragma unroll
-      for (int j = 0; j < RPT; ++j) atomicAdd(&L.hist[key[j] >> hi], 1u);
+      for (int c = 0; c < RCH; ++c) {
+        if (c * RCHUNK < n) {
+#pragma unroll
+          for (int u = 0; u < RCW; ++u) atomicAdd(&L.hist[key[RCW * c + u] >> hi], 1u);
+        }
+      }
+      if (tid == 0 && n < RMAX) atomicAdd(&L.hist[0], uint32_t(RCHUNK * (RCH - (n + RCHUNK - 1) / RCHUNK)));
       __syncthreads();
       if (wave == 0) {
         const Pick p = pick_bucket<SBINS / 64>(L.hist, rem, lane);
