@@ -112,8 +112,8 @@ __device__ __forceinline__ void dma16(const char* vaddr, uint32_t lds) {
 }
 
 // Page numbers of paged-cache slabs (16 keys, which lie in one page because pages hold a
-// power of two >= 16 keys), fetched with scalar loads at the moment they are needed and
-// waited for at once.  At the start of a step no LDS read is outstanding, so the wait
+// power of two >= 16 keys), fetched with scalar loads and waited for at once.  They are
+// loaded where no LDS read is outstanding (the end of a step, or the prologue), so the wait
 // covers only these loads, which hit the scalar cache (16 consecutive table entries per
 // line).  Vector loads of the page numbers would be counted with the tile DMAs, which
 // complete in order: waiting for a page number would wait for every DMA issued before it.
