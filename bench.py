@@ -42,7 +42,7 @@ PEAK_FP8_TFLOPS = 5033.2     # dense E4M3 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
 METRIC = "cached tokens scored/sec per refresh; attention TFLOP/s as % of bf16 MFMA peak"
 DEFAULT_CONFIGS = "C5,C3,C4,C2"
 # rows of the oracle's bounded sample per workload (about 10-30 s of host work each)
-CPU_ROWS = {"C2": 512, "C3": 256, "C5": 512, "C4": 12}
+CPU_ROWS = {"C2": 512, "C3": 256, "C5": 512, "C4": 12, "C2H": 256}
 
 
 def parse():
@@ -98,9 +98,9 @@ def _row_flops(cfg, rows):
     hq, d, D, V = cfg.n_heads_q, cfg.head_dim, cfg.hidden, cfg.vocab
     att = 4.0 * d * hq * keys
     lm = 2.0 * D * V
-    if cfg.mode == "full":
+    if cfg.mode in ("full", "last_layer_h"):
         per_layer = 2.0 * D * hq * d * 2 + 2.0 * D * cfg.ffn * 3
-        return cfg.n_layers * (per_layer + att) + lm
+        return (cfg.n_layers if cfg.mode == "full" else 1) * (per_layer + att) + lm
     return att + 2.0 * D * hq * d + lm
 
 
@@ -128,6 +128,10 @@ def cpu_baseline(w, rows_count: int) -> dict:
                               lambda l: h["layers"][l], h["embed"], h["final_norm"], h["w_lm"],
                               cfg.cu_seqlens, cfg.n_layers, cfg.n_heads_q, cfg.head_dim,
                               cfg.rope_theta, cfg.rms_eps, rows=rows)
+        elif cfg.mode == "last_layer_h":
+            s = O.last_layer_h_scores(h["h_last"], h["ids"], h["k"], h["v"], h["layer"],
+                                      h["final_norm"], h["w_lm"], cfg.cu_seqlens, cfg.n_heads_q,
+                                      cfg.head_dim, cfg.rope_theta, cfg.rms_eps, rows=rows)
         else:
             s = O.last_layer_scores(h["q"], h["k"], h["v"], h["w_o"], h["w_lm"], h["ids"],
                                     cfg.cu_seqlens, rows=rows)
@@ -268,8 +272,9 @@ def _out_cache(w):
 def bench_config(args, name: str, dev, with_extras: bool) -> dict:
     """Whole refreshes of one workload.  Last-layer workloads run as the sub-step chain
     (attention -> W_o -> packed LM head -> select -> compaction), checked once to equal
-    cc_score bit for bit, so each sub-step has its own HIP-event time; the full pass runs
-    as cc_score."""
+    cc_score bit for bit, so each sub-step has its own HIP-event time; the full pass and
+    the exact fast variant (from the stored activations H, which are compacted with the
+    cache) run as cc_score."""
     import torch
     from paper_2607_27600_amd import cc
     from paper_2607_27600_amd.workload import Workload
@@ -302,7 +307,14 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
     ws_cmp = torch.empty(max(1, cc.cc_compact_workspace(p, L, per_head)), dtype=torch.uint8,
                          device=dev)
     out_kv = _out_cache(w)
-    full = cfg.mode == "full"
+    # the exact fast variant also compacts the stored activations H with the cache
+    h_rows = w.h_last if cfg.mode == "last_layer_h" else None
+    if h_rows is not None:
+        out_h = torch.empty_like(h_rows)
+        ws_rows = torch.empty(max(1, cc.cc_compact_rows_workspace(
+            p, h_rows[0].numel() * h_rows.element_size(), per_head)), dtype=torch.uint8, device=dev)
+    # the full pass and the exact fast variant (from the stored activations H) run as cc_score
+    full = cfg.mode in ("full", "last_layer_h")
     o = u = ws_att = None
     if full:
         names = ["score", "select", "compact"]
@@ -332,6 +344,8 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
         cc.cc_select_keep(scores, starts, lens, ks, keep, ws_sel)
         mark(len(names) - 1)
         cc.cc_compact_kv(p, w.kv, keep, ks, per_head, out=out_kv, workspace=ws_cmp)
+        if h_rows is not None:
+            cc.cc_compact_rows(p, h_rows, keep, ks, per_head, out=out_h, workspace=ws_rows)
         mark(len(names))
 
     if args.pmc_driver:
@@ -373,7 +387,9 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
     wo_flop = 2.0 * N * D * Hq * d
     per_layer = 2.0 * N * D * (Hq * d) * 2 + 2.0 * N * D * cfg.ffn * 3
     kept_rows = sum(ks) if per_head else sum(ks) * hkv        # (token, KV head) rows per layer
-    cmp_bytes = 2 * (2 * L * kept_rows * d * 2)               # K and V, read + write
+    kv_bytes = cmp_bytes = 2 * (2 * L * kept_rows * d * 2)    # K and V, read + write
+    if h_rows is not None:                                     # + the stored activations H
+        cmp_bytes += 2 * sum(ks) * h_rows[0].numel() * h_rows.element_size()
 
     res = {"workload": f"{cfg.name}: {cfg.description}", "n_cached": N, "n_seqs": cfg.n_seqs,
            "cache_layers": L, "paged": bool(cfg.paged), "mode": cfg.mode,
@@ -381,12 +397,15 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
            "breakdown_ms": part, "input_generation_s": t_gen,
            "lmhead_layout": {"packed": True, "pack_w_lm_ms": pack_w_ms}}
     if full:
-        score_flop = cfg.n_layers * (per_layer + att_flop) + lm_flop
+        n_pass = cfg.n_layers if cfg.mode == "full" else 1
+        score_flop = n_pass * (per_layer + att_flop) + lm_flop
         achieved = score_flop / (part["score"] * 1e-3) / 1e12
+        what = ("the whole 32-layer score pass (cc_score, FULL)" if cfg.mode == "full" else
+                "the exact fast variant's score pass (cc_score, LAST_LAYER_H: the last layer "
+                "from the stored activations, then the LM head)")
         res["roofline"] = {
-            "kernel": "the whole 32-layer score pass (cc_score, FULL): every kernel in it is a "
-                      "bf16 MFMA contraction (projections, SwiGLU MLP, attention, LM head) or "
-                      "negligible; the largest, the gate/up GEMM, is 45% of the FLOPs",
+            "kernel": what + ": every kernel in it is a bf16 MFMA contraction (projections, "
+                      "SwiGLU MLP, attention, LM head) or negligible",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None, "flop_per_launch": score_flop}
         # attention of one layer at this workload's shape, on its own (synthetic queries)
@@ -443,11 +462,11 @@ def bench_config(args, name: str, dev, with_extras: bool) -> dict:
     ip_ms = ev_ip[0].elapsed_time(ev_ip[1]) / args.steps
     ip_fl = flushed_ms(lambda: cc.cc_compact_kv(p, w.kv, keep, ks, per_head, workspace=ws_cmp),
                        5, flush)
-    res["compact_in_place"] = {"bytes_moved": cmp_bytes, "ms": ip_ms,
-                               "gb_s": cmp_bytes / (ip_ms * 1e-3) / 1e9,
+    res["compact_in_place"] = {"bytes_moved": kv_bytes, "ms": ip_ms,
+                               "gb_s": kv_bytes / (ip_ms * 1e-3) / 1e9,
                                "ms_cache_flushed": ip_fl,
-                               "gb_s_cache_flushed": cmp_bytes / (ip_fl * 1e-3) / 1e9,
-                               "frac_hbm_cache_flushed": cmp_bytes / (ip_fl * 1e-3) / 1e9 / PEAK_HBM_GBS}
+                               "gb_s_cache_flushed": kv_bytes / (ip_fl * 1e-3) / 1e9,
+                               "frac_hbm_cache_flushed": kv_bytes / (ip_fl * 1e-3) / 1e9 / PEAK_HBM_GBS}
     del flush, out_kv
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, CPU_ROWS.get(name, 64))

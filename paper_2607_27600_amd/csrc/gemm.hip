@@ -243,18 +243,31 @@ struct EpiResidual {
     (void)tm;
     (void)lds;
     const int hi = lane >> 5, col = lane & 31;
+    // Per 32-row block: the 16 x GNB residual values are loaded together (rows and columns
+    // clamped, so no load is conditional), then added and stored.  Element by element, each
+    // add waited for its own load: 128 memory round trips per lane.
 #pragma unroll
-    for (int mb = 0; mb < GMB; ++mb)
+    for (int mb = 0; mb < GMB; ++mb) {
+      float r[GNB][16];
+#pragma unroll
+      for (int nb = 0; nb < GNB; ++nb) {
+        const int nc = min(n0w + nb * 32 + col, g.N - 1);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = min(m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3), g.M - 1);
+          r[nb][e] = h[int64_t(m) * g.N + nc];
+        }
+      }
 #pragma unroll
       for (int nb = 0; nb < GNB; ++nb) {
         const int n = n0w + nb * 32 + col;
-        if (n >= g.N) continue;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int m = m0w + mb * 32 + (e >> 2) * 8 + hi * 4 + (e & 3);
-          if (m < g.M) h[int64_t(m) * g.N + n] += acc[mb][nb][e];
+          if (n < g.N && m < g.M) h[int64_t(m) * g.N + n] = r[nb][e] + acc[mb][nb][e];
         }
       }
+    }
   }
 };
 
