@@ -40,7 +40,7 @@ PEAK_BF16_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
 PEAK_FP8_TFLOPS = 5033.2     # dense E4M3 MFMA: 256 CU x 2.4 GHz x 8192 FLOP/clk
 METRIC = "cached tokens scored/sec per refresh; attention TFLOP/s as % of bf16 MFMA peak"
-DEFAULT_CONFIGS = "C5,C3,C4,C2"
+DEFAULT_CONFIGS = "C5,C3,C4,C2,C2H"
 # rows of the oracle's bounded sample per workload (about 10-30 s of host work each)
 CPU_ROWS = {"C2": 512, "C3": 256, "C5": 512, "C4": 12, "C2H": 256}
 
